@@ -1,0 +1,191 @@
+/*
+ * celty.h -- C ABI of libcelty: dual-sparse SpMSpV y = W x on AMD MI355X (gfx950).
+ *
+ * The operation (Celty, Sections 2.1 and 3.1): W is an unstructured-pruned
+ * fp16 weight matrix (M rows = outputs, K columns = inputs) kept in the
+ * paper's run-length compressed CSC format (RLC-CSC, Section 3.2); x is an
+ * fp16 activation vector made sparse at run time by magnitude thresholding
+ * (Sections 1 and 2.1): column k takes part iff |x_k| > tau.  Then
+ *
+ *     y[r] = sum over active k of W[r,k] * x_k,     r = 0 .. M-1,
+ *
+ * with fp32 products and fp32 accumulation (Section 5) and y rounded to fp16
+ * (round to nearest even).  Inactive columns of W are never read (Section 3.1).
+ *
+ * General rules
+ * -------------
+ * - No function allocates or frees caller-visible memory.  Every buffer is
+ *   owned by the caller.  The encoder uses small per-thread host scratch.
+ * - No C++ exception crosses this interface; every error is a status code.
+ * - Host pointers and device pointers are marked at each argument.
+ * - Device calls (celty_select, celty_spmspv*) validate every argument on the
+ *   host, synchronously, before any launch; they then enqueue work on the
+ *   given HIP stream (NULL = the default stream) and return without
+ *   synchronising.  They are stateless: calls on different streams may run
+ *   concurrently when their output and workspace buffers differ.
+ */
+#ifndef CELTY_H
+#define CELTY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum celty_status {
+  CELTY_OK = 0,
+  CELTY_EINVAL = 1,     /* bad argument: null pointer, bad size, NaN tau, short buffer, misalignment */
+  CELTY_ENOMEM = 2,     /* host scratch or worker threads could not be created */
+  CELTY_EOVERFLOW = 3,  /* the encoded group count does not fit in uint32 */
+  CELTY_EFORMAT = 4,    /* malformed RLC-CSC stream (decoder only) */
+  CELTY_EHIP = 5        /* the HIP runtime reported an error at launch */
+} celty_status;
+
+#define CELTY_FORMAT_VERSION 1
+#define CELTY_RUN_BITS 4   /* 4-bit run lengths (Section 3.2) */
+#define CELTY_GROUP 8      /* entries per aligned group: one 16-byte fp16 vector */
+
+/*
+ * Tiled RLC-CSC, format version 1 (Section 3.2 plus the readings below).
+ *
+ * Rows are cut into T = ceil(M/R) tiles of R rows.  Segment (t, k) holds the
+ * stored entries of column k inside tile t; segments are laid out tile-major,
+ * s = t*K + k, so the segments one row tile needs are contiguous.
+ *  - A weight is stored iff it is kept by the mask and is not +0/-0.
+ *  - Each stored value carries a 4-bit run: the count of zeros since the
+ *    previous stored entry of the segment, or since the tile's first row.
+ *  - A gap g > 15 is bridged greedily: g/16 padding entries (value 0, run 15)
+ *    come first, then the value with run g%16 (the worked example of 3.2).
+ *    Trailing zeros are not encoded.
+ *  - Row of entry i of a segment = t*R + (sum of runs 0..i) + i (Section 3.3).
+ *  - Each segment is padded to a multiple of 8 entries with (0, 0) "dead"
+ *    entries, so every segment starts on a 16-byte boundary.
+ *  - values[8g + j] is the fp16 bit pattern of entry j of group g; runs[g]
+ *    holds entry j's run in bits [4j, 4j+4).
+ *  - gptr[s] is the first group of segment s; gptr[T*K] = n_groups.
+ * The descriptor is plain data; the three arrays are owned by the caller and
+ * are host pointers for the encoder/decoder and device pointers for
+ * celty_spmspv*.
+ */
+typedef struct celty_rlc_csc {
+  int32_t version;          /* CELTY_FORMAT_VERSION */
+  int32_t M, K, R, T;       /* rows (outputs), columns (inputs), tile rows, ceil(M/R) */
+  int32_t run_bits;         /* CELTY_RUN_BITS */
+  int64_t n_groups;         /* G: 8-entry groups, alignment included */
+  int64_t n_entries;        /* stored values + padding entries (alignment excluded) */
+  int64_t n_nnz;            /* stored values */
+  int64_t n_pad;            /* padding entries */
+  const uint32_t* gptr;     /* [T*K + 1], 4-byte aligned */
+  const uint16_t* values;   /* [8*G] fp16 bits, 16-byte aligned */
+  const uint32_t* runs;     /* [G], 4-byte aligned */
+} celty_rlc_csc;
+
+/*
+ * Size plan of the encoding of a dense fp16 matrix under a keep-mask (Section
+ * 3.2, offline packing).
+ *   W      host, fp16 bit patterns, row-major M x K with row stride ldw >= K.
+ *   mask   host, uint8 row-major with row stride ldm >= K; non-zero = kept.
+ *          NULL keeps every entry (then only +-0 weights are dropped).
+ *   R      tile height, 1 <= R; T = ceil(M/R).
+ * Outputs (host, may not be NULL): n_groups, n_nnz, n_pad.
+ * Errors: EINVAL (null W or output pointer, M/K/R < 1, short stride),
+ *         EOVERFLOW (n_groups > UINT32_MAX), ENOMEM.
+ */
+celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm,
+                               int32_t M, int32_t K, int32_t R,
+                               int64_t* n_groups, int64_t* n_nnz, int64_t* n_pad);
+
+/*
+ * Encode into caller buffers (host): gptr [T*K+1], values [8*n_groups]
+ * (16-byte aligned), runs [n_groups].  n_groups must equal the plan's value.
+ * On success *out is filled (pointers = the three buffers given here).
+ * n_threads: worker threads, 0 = all hardware threads.  The result does not
+ * depend on n_threads.
+ * Errors: EINVAL (as for the plan, null buffers, misaligned values,
+ *         n_groups mismatch, n_threads < 0), EOVERFLOW, ENOMEM.
+ */
+celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm,
+                          int32_t M, int32_t K, int32_t R,
+                          uint32_t* gptr, uint16_t* values, uint32_t* runs, int64_t n_groups,
+                          celty_rlc_csc* out, int32_t n_threads);
+
+/*
+ * Decode a format-v1 stream held in host memory back to dense form (host).
+ *   W_out    host, M x K fp16 bits, row-major, stride K: stored values, +0 elsewhere.
+ *   mask_out host, M x K uint8, stride K: 1 where a value is stored (may be NULL).
+ * Errors: EINVAL (null pointers, bad header), EFORMAT (gptr not monotone from
+ * 0 to n_groups, a stored value beyond its tile, an alignment entry with a
+ * non-zero run, header counts that disagree with the stream).
+ */
+celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out);
+
+/*
+ * Active-column selection (Sections 1, 2.1 and 3.1: magnitude threshold,
+ * then stream compaction by wavefront ballot and prefix sums).
+ *   x      device, fp16[K].
+ *   tau    threshold; column k is active iff |x_k| > tau in fp32 (NaN x_k is
+ *          never active; tau < 0 makes every non-NaN column active).
+ *   idx    device, int32[K]: receives the active indices in ascending order.
+ *   count  device, int32[1]: receives |A|.
+ * Errors: EINVAL (null pointers, K < 1, NaN tau, misaligned idx/count), EHIP.
+ */
+celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int32_t* count,
+                          void* stream);
+
+/* Launch shape of celty_spmspv_ex.  Zero fields mean "choose automatically". */
+typedef struct celty_launch {
+  int32_t cols_per_block;   /* columns of x one workgroup scans (1..4096) */
+  int32_t waves_per_block;  /* 2, 4, 8 or 16 wavefronts of 64 lanes */
+} celty_launch;
+
+/* Bytes of device workspace celty_spmspv needs for this shape (M floats of
+ * partial sums plus T counters, each rounded to 256 bytes). */
+size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R);
+
+/*
+ * Zero-fill a workspace (device) on `stream`.  A workspace must be zero-filled
+ * once before its first use; every completed celty_spmspv call leaves it
+ * zero-filled again.  Errors: EINVAL (null), EHIP.
+ */
+celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The dual-sparse SpMSpV (Sections 3.1-3.3): y = W x_A.
+ *   W          descriptor with DEVICE pointers (format v1, e.g. the encoder's
+ *              arrays copied to the device); must be a valid encoder output.
+ *   x          device fp16[K]; must be finite (an infinite x_k is outside the
+ *              operation's domain and yields unspecified rows).
+ *   tau        threshold, as for celty_select.
+ *   y          device fp16[M]; fully overwritten (rows without contribution
+ *              become +0); must not alias x or the workspace.
+ *   workspace  device buffer of at least celty_spmspv_workspace_bytes(M,K,R)
+ *              bytes, zero-filled before first use (celty_spmspv_workspace_init).
+ * One kernel launch: every workgroup selects the active columns of its slice
+ * of x, walks their compressed segments for its row tile, accumulates fp32
+ * partial products in LDS and merges tile partials across workgroups.
+ * Errors: EINVAL (null or misaligned pointers, inconsistent header, NaN tau,
+ *         short workspace), EHIP.
+ */
+celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* As celty_spmspv with an explicit launch shape (NULL = automatic). */
+celty_status celty_spmspv_ex(const celty_rlc_csc* W, const void* x, float tau, void* y,
+                             void* workspace, size_t workspace_bytes,
+                             const celty_launch* launch, void* stream);
+
+/* The launch shape celty_spmspv_ex would use for W and `launch` (host only):
+ * fills *resolved and, if not NULL, the workgroup count and LDS bytes. */
+celty_status celty_spmspv_plan(const celty_rlc_csc* W, const celty_launch* launch,
+                               celty_launch* resolved, int64_t* n_blocks, int64_t* lds_bytes);
+
+/* Static text for a status code. */
+const char* celty_status_string(celty_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CELTY_H */

@@ -1,0 +1,278 @@
+"""Dual-sparse SpMSpV for AMD MI355X: Python binding of libcelty (include/celty.h).
+
+The functions below carry the C names and only marshal arguments: numpy
+arrays for the host encoder/decoder, torch tensors for device memory and
+``torch.cuda`` streams for ordering.  All arithmetic of the product runs in
+the HIP kernels of libcelty.so; there is no fallback path.  Importing this
+package fails loudly if the library has not been built
+(``python paper_2608_01536_amd/build_lib.py``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcelty.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is not built; run `python paper_2608_01536_amd/build_lib.py`")
+_lib = ctypes.CDLL(_LIB_PATH)
+
+CELTY_OK, CELTY_EINVAL, CELTY_ENOMEM, CELTY_EOVERFLOW, CELTY_EFORMAT, CELTY_EHIP = range(6)
+FORMAT_VERSION = 1
+RUN_BITS = 4
+GROUP = 8
+
+_p = ctypes.c_void_p
+_i32, _i64, _f32, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+
+
+class celty_rlc_csc(ctypes.Structure):
+    _fields_ = [("version", _i32), ("M", _i32), ("K", _i32), ("R", _i32), ("T", _i32),
+                ("run_bits", _i32), ("n_groups", _i64), ("n_entries", _i64), ("n_nnz", _i64),
+                ("n_pad", _i64), ("gptr", _p), ("values", _p), ("runs", _p)]
+
+
+class celty_launch(ctypes.Structure):
+    _fields_ = [("cols_per_block", _i32), ("waves_per_block", _i32)]
+
+
+def _sig(name, res, *args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = list(args)
+    return f
+
+
+_encode_plan = _sig("celty_encode_plan", ctypes.c_int, _p, _i64, _p, _i64, _i32, _i32, _i32,
+                    ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.POINTER(_i64))
+_encode = _sig("celty_encode", ctypes.c_int, _p, _i64, _p, _i64, _i32, _i32, _i32, _p, _p, _p, _i64,
+               ctypes.POINTER(celty_rlc_csc), _i32)
+_decode = _sig("celty_decode", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _p)
+_select = _sig("celty_select", ctypes.c_int, _p, _i32, _f32, _p, _p, _p)
+_ws_bytes = _sig("celty_spmspv_workspace_bytes", _sz, _i32, _i32, _i32)
+_ws_init = _sig("celty_spmspv_workspace_init", ctypes.c_int, _p, _sz, _p)
+_spmspv = _sig("celty_spmspv", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz, _p)
+_spmspv_ex = _sig("celty_spmspv_ex", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz,
+                  ctypes.POINTER(celty_launch), _p)
+_plan = _sig("celty_spmspv_plan", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), ctypes.POINTER(celty_launch),
+             ctypes.POINTER(celty_launch), ctypes.POINTER(_i64), ctypes.POINTER(_i64))
+_status_string = _sig("celty_status_string", ctypes.c_char_p, ctypes.c_int)
+
+
+class CeltyError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {celty_status_string(status)}")
+
+
+def celty_status_string(status: int) -> str:
+    return _status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != CELTY_OK:
+        raise CeltyError(status, where)
+
+
+def _aligned_empty(n: int, dtype, align: int = 64) -> np.ndarray:
+    dt = np.dtype(dtype)
+    raw = np.empty(n * dt.itemsize + align, dtype=np.uint8)
+    off = (-raw.ctypes.data) % align
+    return raw[off:off + n * dt.itemsize].view(dt)
+
+
+def _host_matrix(W: np.ndarray, mask):
+    Wb = np.ascontiguousarray(np.asarray(W)).view(np.uint16)
+    if Wb.ndim != 2:
+        raise ValueError("W must be 2-D (M x K)")
+    if mask is None:
+        return Wb, None
+    m = np.ascontiguousarray(np.asarray(mask)).astype(np.uint8, copy=False)
+    if m.shape != Wb.shape:
+        raise ValueError("mask must have W's shape")
+    return Wb, m
+
+
+# ---------------------------------------------------------------------------
+# Host encoder / decoder
+# ---------------------------------------------------------------------------
+class HostRlcCsc:
+    """Format-v1 arrays in host memory plus the header."""
+
+    def __init__(self, desc: celty_rlc_csc, gptr: np.ndarray, values: np.ndarray, runs: np.ndarray):
+        self.M, self.K, self.R, self.T = desc.M, desc.K, desc.R, desc.T
+        self.n_groups, self.n_entries = int(desc.n_groups), int(desc.n_entries)
+        self.n_nnz, self.n_pad = int(desc.n_nnz), int(desc.n_pad)
+        self.gptr, self.values, self.runs = gptr, values, runs
+
+    def desc(self) -> celty_rlc_csc:
+        return celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
+                             self.n_entries, self.n_nnz, self.n_pad, self.gptr.ctypes.data,
+                             self.values.ctypes.data if self.values.size else None,
+                             self.runs.ctypes.data if self.runs.size else None)
+
+    def to_device(self, device=None) -> "DeviceRlcCsc":
+        return DeviceRlcCsc(self, device)
+
+
+def celty_encode_plan(W: np.ndarray, mask, R: int) -> Tuple[int, int, int]:
+    Wb, m = _host_matrix(W, mask)
+    M, K = Wb.shape
+    g, n, p = _i64(), _i64(), _i64()
+    _check(_encode_plan(Wb.ctypes.data, K, None if m is None else m.ctypes.data, K, M, K, int(R),
+                        ctypes.byref(g), ctypes.byref(n), ctypes.byref(p)), "celty_encode_plan")
+    return g.value, n.value, p.value
+
+
+def celty_encode(W: np.ndarray, mask, R: int, n_threads: int = 0) -> HostRlcCsc:
+    """fp16 W (M x K) + keep-mask -> format v1 in fresh host arrays."""
+    Wb, m = _host_matrix(W, mask)
+    M, K = Wb.shape
+    G, _, _ = celty_encode_plan(Wb, m, R)
+    T = -(-M // int(R))
+    gptr = _aligned_empty(T * K + 1, np.uint32)
+    values = _aligned_empty(GROUP * G, np.uint16)
+    runs = _aligned_empty(G, np.uint32)
+    desc = celty_rlc_csc()
+    _check(_encode(Wb.ctypes.data, K, None if m is None else m.ctypes.data, K, M, K, int(R),
+                   gptr.ctypes.data, values.ctypes.data, runs.ctypes.data, G, ctypes.byref(desc),
+                   int(n_threads)), "celty_encode")
+    return HostRlcCsc(desc, gptr, values, runs)
+
+
+def celty_decode(enc: HostRlcCsc) -> Tuple[np.ndarray, np.ndarray]:
+    W = np.empty((enc.M, enc.K), dtype=np.uint16)
+    mask = np.empty((enc.M, enc.K), dtype=np.uint8)
+    d = enc.desc()
+    _check(_decode(ctypes.byref(d), W.ctypes.data, mask.ctypes.data), "celty_decode")
+    return W.view(np.float16), mask
+
+
+# ---------------------------------------------------------------------------
+# Device side (torch supplies memory and streams)
+# ---------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream) -> Optional[int]:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev_ptr(t, nbytes_each: int, name: str) -> int:
+    if not t.is_cuda or not t.is_contiguous() or t.element_size() != nbytes_each:
+        raise ValueError(f"{name} must be a contiguous CUDA tensor of {nbytes_each}-byte elements")
+    return int(t.data_ptr())
+
+
+class DeviceRlcCsc:
+    """Format-v1 arrays copied into device tensors, plus a device descriptor."""
+
+    def __init__(self, host: HostRlcCsc, device=None):
+        torch = _torch()
+        device = torch.device("cuda") if device is None else torch.device(device)
+        self.host_header = host
+        self.M, self.K, self.R, self.T = host.M, host.K, host.R, host.T
+        self.n_groups, self.n_entries = host.n_groups, host.n_entries
+        self.n_nnz, self.n_pad = host.n_nnz, host.n_pad
+        self.gptr = torch.from_numpy(host.gptr.view(np.int32)).to(device)
+        # at least one element so that pointers are never null
+        self.values = torch.from_numpy(host.values.view(np.int16) if host.values.size
+                                       else np.zeros(8, np.int16)).to(device)
+        self.runs = torch.from_numpy(host.runs.view(np.int32) if host.runs.size
+                                     else np.zeros(1, np.int32)).to(device)
+        self._desc = celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
+                                   self.n_entries, self.n_nnz, self.n_pad, self.gptr.data_ptr(),
+                                   self.values.data_ptr(), self.runs.data_ptr())
+
+    def desc(self) -> celty_rlc_csc:
+        return self._desc
+
+    def clone_to(self, device=None) -> "DeviceRlcCsc":
+        """A second copy of the arrays at new device addresses."""
+        other = object.__new__(DeviceRlcCsc)
+        other.__dict__.update(self.__dict__)
+        other.gptr, other.values, other.runs = self.gptr.clone(), self.values.clone(), self.runs.clone()
+        other._desc = celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
+                                    self.n_entries, self.n_nnz, self.n_pad, other.gptr.data_ptr(),
+                                    other.values.data_ptr(), other.runs.data_ptr())
+        return other
+
+
+def celty_spmspv_workspace_bytes(M: int, K: int, R: int) -> int:
+    return int(_ws_bytes(int(M), int(K), int(R)))
+
+
+def celty_spmspv_workspace_init(workspace, stream=None) -> None:
+    _check(_ws_init(_dev_ptr(workspace, 1, "workspace"), workspace.numel(), _stream_handle(stream)),
+           "celty_spmspv_workspace_init")
+
+
+def new_workspace(W: DeviceRlcCsc, device=None):
+    """A zero-filled device workspace for W's shape (uint8 tensor)."""
+    torch = _torch()
+    n = celty_spmspv_workspace_bytes(W.M, W.K, W.R)
+    return torch.zeros(n, dtype=torch.uint8, device=device if device is not None else W.gptr.device)
+
+
+def celty_select(x, tau: float, idx, count, stream=None) -> None:
+    K = x.numel()
+    _check(_select(_dev_ptr(x, 2, "x"), K, float(tau), _dev_ptr(idx, 4, "idx"), _dev_ptr(count, 4, "count"),
+                   _stream_handle(stream)), "celty_select")
+
+
+def _launch_struct(launch) -> Optional[celty_launch]:
+    if launch is None:
+        return None
+    if isinstance(launch, celty_launch):
+        return launch
+    cols, waves = launch
+    return celty_launch(int(cols), int(waves))
+
+
+def celty_spmspv(W: DeviceRlcCsc, x, tau: float, y, workspace, stream=None) -> None:
+    d = W.desc()
+    _check(_spmspv(ctypes.byref(d), _dev_ptr(x, 2, "x"), float(tau), _dev_ptr(y, 2, "y"),
+                   _dev_ptr(workspace, 1, "workspace"), workspace.numel(), _stream_handle(stream)),
+           "celty_spmspv")
+
+
+def celty_spmspv_ex(W: DeviceRlcCsc, x, tau: float, y, workspace, launch=None, stream=None) -> None:
+    d = W.desc()
+    ls = _launch_struct(launch)
+    _check(_spmspv_ex(ctypes.byref(d), _dev_ptr(x, 2, "x"), float(tau), _dev_ptr(y, 2, "y"),
+                      _dev_ptr(workspace, 1, "workspace"), workspace.numel(),
+                      None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_ex")
+
+
+def celty_spmspv_plan(W, launch=None) -> dict:
+    d = W.desc()
+    ls = _launch_struct(launch)
+    out, nb, lds = celty_launch(), _i64(), _i64()
+    _check(_plan(ctypes.byref(d), None if ls is None else ctypes.byref(ls), ctypes.byref(out),
+                 ctypes.byref(nb), ctypes.byref(lds)), "celty_spmspv_plan")
+    return dict(cols_per_block=out.cols_per_block, waves_per_block=out.waves_per_block,
+                blocks=nb.value, lds_bytes=lds.value)
+
+
+def default_tile_rows(M: int, K: int) -> int:
+    """Tile height R used for the benchmark encodings (rows per LDS tile).
+
+    256 rows keep segments short enough for row-tile parallelism on 256 CUs
+    while the 8-entry alignment costs only a few percent of the bytes."""
+    return 256
+
+
+__all__ = [
+    "default_tile_rows",
+    "celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv", "celty_spmspv_ex",
+    "celty_spmspv_plan", "celty_spmspv_workspace_bytes", "celty_spmspv_workspace_init", "celty_status_string",
+    "new_workspace", "HostRlcCsc", "DeviceRlcCsc", "CeltyError", "celty_rlc_csc", "celty_launch",
+]

@@ -1,0 +1,275 @@
+// Host RLC-CSC encoder and decoder (offline packing, Section 3.2).
+//
+// Work is split into items (row tile t, block of columns); an item walks the
+// rows of its tile in memory order, keeping per-column state, so W and the
+// mask are read row-major and contiguously.  Segments of one item are
+// contiguous in the tile-major layout, so items never write the same bytes
+// and the output does not depend on the thread count.
+
+#include <algorithm>
+#include <atomic>
+#include <cstring>
+#include <new>
+#include <thread>
+#include <vector>
+
+#include "celty.h"
+
+namespace {
+
+constexpr int kCap = (1 << CELTY_RUN_BITS) - 1;   // largest run a padding entry carries
+constexpr int kColBlock = 512;                      // columns per work item
+
+inline bool stored(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm, int64_t r,
+                   int64_t k) {
+  if ((W[r * ldw + k] & 0x7FFFu) == 0) return false;   // +0 / -0 are never stored
+  return mask == nullptr || mask[r * ldm + k] != 0;
+}
+
+struct Item {
+  int32_t t, k0, k1;
+};
+
+std::vector<Item> make_items(int32_t T, int32_t K) {
+  std::vector<Item> items;
+  for (int32_t t = 0; t < T; ++t)
+    for (int32_t k0 = 0; k0 < K; k0 += kColBlock) items.push_back({t, k0, std::min(K, k0 + kColBlock)});
+  return items;
+}
+
+// Runs fn(item_index) over all items on n_threads workers.  Returns false if
+// a worker could not be started (the caller maps this to ENOMEM).
+template <class Fn>
+bool parallel_items(size_t n_items, int32_t n_threads, Fn fn) {
+  unsigned hw = std::thread::hardware_concurrency();
+  size_t nt = n_threads > 0 ? size_t(n_threads) : size_t(hw ? hw : 1);
+  nt = std::max<size_t>(1, std::min(nt, n_items));
+  std::atomic<size_t> next{0};
+  auto worker = [&]() {
+    for (size_t i = next.fetch_add(1); i < n_items; i = next.fetch_add(1)) fn(i);
+  };
+  std::vector<std::thread> pool;
+  try {
+    for (size_t i = 1; i < nt; ++i) pool.emplace_back(worker);
+  } catch (...) {
+    for (auto& th : pool) th.join();
+    return false;
+  }
+  worker();
+  for (auto& th : pool) th.join();
+  return true;
+}
+
+// Counts entries per segment of one item; writes groups per segment into
+// seg_groups (indexed s - (t*K + k0)) when non-null and adds the totals.
+void count_item(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm, int32_t M,
+                int32_t R, const Item& it, std::vector<int32_t>& last, std::vector<int64_t>& cnt,
+                int64_t& nnz, int64_t& pad, int64_t& groups, uint32_t* seg_groups) {
+  const int32_t nk = it.k1 - it.k0;
+  const int64_t r0 = int64_t(it.t) * R, r1 = std::min<int64_t>(M, r0 + R);
+  std::fill(last.begin(), last.begin() + nk, -1);
+  std::fill(cnt.begin(), cnt.begin() + nk, 0);
+  for (int64_t r = r0; r < r1; ++r) {
+    const int32_t rel = int32_t(r - r0);
+    for (int32_t j = 0; j < nk; ++j) {
+      if (!stored(W, ldw, mask, ldm, r, it.k0 + j)) continue;
+      const int32_t gap = rel - last[j] - 1;
+      cnt[j] += gap / (kCap + 1) + 1;
+      pad += gap / (kCap + 1);
+      ++nnz;
+      last[j] = rel;
+    }
+  }
+  for (int32_t j = 0; j < nk; ++j) {
+    const int64_t g = (cnt[j] + CELTY_GROUP - 1) / CELTY_GROUP;
+    groups += g;
+    if (seg_groups) seg_groups[j] = uint32_t(g);
+  }
+}
+
+celty_status check_common(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm,
+                          int32_t M, int32_t K, int32_t R) {
+  if (!W || M < 1 || K < 1 || R < 1 || ldw < K) return CELTY_EINVAL;
+  if (mask && ldm < K) return CELTY_EINVAL;
+  return CELTY_OK;
+}
+
+}  // namespace
+
+extern "C" celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const uint8_t* mask,
+                                          int64_t ldm, int32_t M, int32_t K, int32_t R,
+                                          int64_t* n_groups, int64_t* n_nnz, int64_t* n_pad) {
+  if (!n_groups || !n_nnz || !n_pad) return CELTY_EINVAL;
+  if (celty_status st = check_common(W, ldw, mask, ldm, M, K, R)) return st;
+  try {
+    const int32_t T = int32_t((int64_t(M) + R - 1) / R);
+    const std::vector<Item> items = make_items(T, K);
+    std::vector<int64_t> nnz(items.size()), pad(items.size()), grp(items.size());
+    bool ok = parallel_items(items.size(), 0, [&](size_t i) {
+      std::vector<int32_t> last(kColBlock);
+      std::vector<int64_t> cnt(kColBlock);
+      int64_t a = 0, b = 0, c = 0;
+      count_item(W, ldw, mask, ldm, M, R, items[i], last, cnt, a, b, c, nullptr);
+      nnz[i] = a;
+      pad[i] = b;
+      grp[i] = c;
+    });
+    if (!ok) return CELTY_ENOMEM;
+    int64_t A = 0, B = 0, C = 0;
+    for (size_t i = 0; i < items.size(); ++i) {
+      A += nnz[i];
+      B += pad[i];
+      C += grp[i];
+    }
+    if (C > int64_t(UINT32_MAX)) return CELTY_EOVERFLOW;
+    *n_groups = C;
+    *n_nnz = A;
+    *n_pad = B;
+    return CELTY_OK;
+  } catch (const std::bad_alloc&) {
+    return CELTY_ENOMEM;
+  } catch (...) {
+    return CELTY_ENOMEM;
+  }
+}
+
+extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8_t* mask,
+                                     int64_t ldm, int32_t M, int32_t K, int32_t R, uint32_t* gptr,
+                                     uint16_t* values, uint32_t* runs, int64_t n_groups,
+                                     celty_rlc_csc* out, int32_t n_threads) {
+  if (celty_status st = check_common(W, ldw, mask, ldm, M, K, R)) return st;
+  if (!gptr || !out || n_threads < 0 || n_groups < 0) return CELTY_EINVAL;
+  if (n_groups > 0 && (!values || !runs)) return CELTY_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(values) & 15u) || (reinterpret_cast<uintptr_t>(runs) & 3u) ||
+      (reinterpret_cast<uintptr_t>(gptr) & 3u))
+    return CELTY_EINVAL;
+  if (n_groups > int64_t(UINT32_MAX)) return CELTY_EOVERFLOW;
+  try {
+    const int32_t T = int32_t((int64_t(M) + R - 1) / R);
+    const int64_t nseg = int64_t(T) * K;
+    const std::vector<Item> items = make_items(T, K);
+    std::vector<int64_t> nnz(items.size()), pad(items.size());
+
+    // pass 1: groups per segment, written into gptr[s] (then scanned in place)
+    bool ok = parallel_items(items.size(), n_threads, [&](size_t i) {
+      const Item& it = items[i];
+      std::vector<int32_t> last(kColBlock);
+      std::vector<int64_t> cnt(kColBlock);
+      int64_t a = 0, b = 0, c = 0;
+      count_item(W, ldw, mask, ldm, M, R, it, last, cnt, a, b, c, gptr + int64_t(it.t) * K + it.k0);
+      nnz[i] = a;
+      pad[i] = b;
+    });
+    if (!ok) return CELTY_ENOMEM;
+    int64_t acc = 0;
+    for (int64_t s = 0; s < nseg; ++s) {
+      const int64_t g = gptr[s];
+      gptr[s] = uint32_t(acc);
+      acc += g;
+      if (acc > int64_t(UINT32_MAX)) return CELTY_EOVERFLOW;
+    }
+    if (acc != n_groups) return CELTY_EINVAL;
+    gptr[nseg] = uint32_t(acc);
+
+    // pass 2: fill.  Each item owns groups [gptr[t*K+k0], gptr[t*K+k1]).
+    ok = parallel_items(items.size(), n_threads, [&](size_t i) {
+      const Item& it = items[i];
+      const int32_t nk = it.k1 - it.k0;
+      const int64_t sbase = int64_t(it.t) * K + it.k0;
+      const int64_t g0 = gptr[sbase], g1 = gptr[sbase + nk];
+      std::memset(values + g0 * CELTY_GROUP, 0, size_t(g1 - g0) * CELTY_GROUP * sizeof(uint16_t));
+      std::memset(runs + g0, 0, size_t(g1 - g0) * sizeof(uint32_t));
+      std::vector<int32_t> last(nk, -1);
+      std::vector<int64_t> pos(nk);   // next entry index (absolute) of each segment
+      for (int32_t j = 0; j < nk; ++j) pos[j] = int64_t(gptr[sbase + j]) * CELTY_GROUP;
+      auto emit = [&](int32_t j, uint16_t v, uint32_t run) {
+        const int64_t e = pos[j]++;
+        values[e] = v;
+        runs[e / CELTY_GROUP] |= run << (4 * (e % CELTY_GROUP));
+      };
+      const int64_t r0 = int64_t(it.t) * R, r1 = std::min<int64_t>(M, r0 + R);
+      for (int64_t r = r0; r < r1; ++r) {
+        const int32_t rel = int32_t(r - r0);
+        for (int32_t j = 0; j < nk; ++j) {
+          if (!stored(W, ldw, mask, ldm, r, it.k0 + j)) continue;
+          int32_t gap = rel - last[j] - 1;
+          while (gap > kCap) {          // padding first, carrying the largest run
+            emit(j, 0, uint32_t(kCap));
+            gap -= kCap + 1;
+          }
+          emit(j, W[r * ldw + it.k0 + j], uint32_t(gap));
+          last[j] = rel;
+        }
+      }
+      // alignment entries (0, 0) are already in place from the memset
+    });
+    if (!ok) return CELTY_ENOMEM;
+
+    int64_t A = 0, B = 0;
+    for (size_t i = 0; i < items.size(); ++i) {
+      A += nnz[i];
+      B += pad[i];
+    }
+    out->version = CELTY_FORMAT_VERSION;
+    out->M = M;
+    out->K = K;
+    out->R = R;
+    out->T = T;
+    out->run_bits = CELTY_RUN_BITS;
+    out->n_groups = n_groups;
+    out->n_entries = A + B;
+    out->n_nnz = A;
+    out->n_pad = B;
+    out->gptr = gptr;
+    out->values = values;
+    out->runs = runs;
+    return CELTY_OK;
+  } catch (...) {
+    return CELTY_ENOMEM;
+  }
+}
+
+extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out) {
+  if (!enc || !W_out) return CELTY_EINVAL;
+  if (enc->version != CELTY_FORMAT_VERSION || enc->run_bits != CELTY_RUN_BITS) return CELTY_EINVAL;
+  const int32_t M = enc->M, K = enc->K, R = enc->R, T = enc->T;
+  if (M < 1 || K < 1 || R < 1 || T != int32_t((int64_t(M) + R - 1) / R) || enc->n_groups < 0)
+    return CELTY_EINVAL;
+  if (!enc->gptr || (enc->n_groups > 0 && (!enc->values || !enc->runs))) return CELTY_EINVAL;
+  const int64_t nseg = int64_t(T) * K;
+  const uint32_t* gptr = enc->gptr;
+  if (gptr[0] != 0 || int64_t(gptr[nseg]) != enc->n_groups) return CELTY_EFORMAT;
+  for (int64_t s = 0; s < nseg; ++s)
+    if (gptr[s + 1] < gptr[s]) return CELTY_EFORMAT;
+  std::memset(W_out, 0, size_t(M) * K * sizeof(uint16_t));
+  if (mask_out) std::memset(mask_out, 0, size_t(M) * K);
+  int64_t nnz = 0, pad = 0;
+  for (int64_t s = 0; s < nseg; ++s) {
+    const int64_t t = s / K, k = s % K;
+    const int64_t hi = std::min<int64_t>(M, (t + 1) * int64_t(R));
+    int64_t row = t * int64_t(R) - 1;
+    int64_t e0 = int64_t(gptr[s]) * CELTY_GROUP, e1 = int64_t(gptr[s + 1]) * CELTY_GROUP;
+    int64_t last_real = e0 - 1;
+    for (int64_t e = e0; e < e1; ++e)
+      if (enc->values[e] & 0x7FFFu) last_real = e;
+    for (int64_t e = e0; e < e1; ++e) {
+      const uint32_t run = (enc->runs[e / CELTY_GROUP] >> (4 * (e % CELTY_GROUP))) & 0xFu;
+      const uint16_t v = enc->values[e];
+      row += int64_t(run) + 1;
+      if (e > last_real) {            // alignment entries must be (0, 0)
+        if (run != 0 || v != 0) return CELTY_EFORMAT;
+        continue;
+      }
+      if (v & 0x7FFFu) {
+        if (row >= hi) return CELTY_EFORMAT;
+        W_out[row * K + k] = v;
+        if (mask_out) mask_out[row * K + k] = 1;
+        ++nnz;
+      } else {
+        ++pad;
+      }
+    }
+  }
+  if (nnz != enc->n_nnz || pad != enc->n_pad || nnz + pad != enc->n_entries) return CELTY_EFORMAT;
+  return CELTY_OK;
+}

@@ -1,0 +1,480 @@
+// Dual-sparse SpMSpV kernels for gfx950 (CDNA4) and their C ABI entry points.
+//
+// One launch computes y = W x_A (Sections 3.1-3.3):
+//   * grid = (row tile t) x (slice c of x).  A workgroup selects the active
+//     columns of its slice (|x_k| > tau, wavefront ballot + prefix sums,
+//     Section 3.1's column skip turned into stream compaction) and drops
+//     columns whose segment in tile t is empty;
+//   * the workgroup's compressed groups (8 entries = 16 B of fp16 values +
+//     4 B of packed 4-bit runs) form one flat sequence; it is cut at segment
+//     boundaries into one contiguous range per wavefront;
+//   * a wavefront walks its range 64 groups (512 entries) per pass: each lane
+//     loads one group with a 128-bit and a 32-bit load (Section 3.1), turns
+//     the 8 runs into 8 inclusive prefixes with byte-packed arithmetic,
+//     combines lanes with a wavefront inclusive scan that restarts at segment
+//     heads (Algorithm 1: prefix of runs plus ordinal gives the row), and
+//     adds value * x_k in fp32 into an LDS tile of the R output rows
+//     (Section 3.3: scatter-accumulation in on-chip memory);
+//   * the tile is merged across slices with fp32 atomics into a workspace row
+//     block; the last workgroup of a row tile (counter) writes y in fp16 and
+//     clears its workspace rows and counter for the next call.  With a single
+//     slice the tile goes straight to y.
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "celty.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
+
+struct SegInfo {
+  uint32_t gstart;   // first group of the segment in the values/runs arrays
+  uint32_t off;      // first group of the segment in the workgroup's flat sequence
+  uint32_t cnt;      // groups in the segment (> 0)
+  float xv;          // x_k as fp32
+};
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t bits) {
+  return __half2float(__ushort_as_half(static_cast<unsigned short>(bits)));
+}
+
+__device__ __forceinline__ unsigned short float_to_half_bits(float v) {
+  return __half_as_ushort(__float2half_rn(v));
+}
+
+// Inclusive scan over the 64 lanes of a wavefront (DPP row shifts inside each
+// 16-lane row, then row broadcasts of lanes 15 and 31).
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);   // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);   // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);   // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);   // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);   // row_bcast:15 -> rows 1, 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);   // row_bcast:31 -> rows 2, 3
+  return v;
+}
+
+// Orders LDS writes of some lanes before LDS reads of other lanes of the
+// same wavefront.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+// LDS slot of a tile-relative row.  Rows past the tile (alignment entries of
+// a segment's last group, value 0) land in the slack; anything out of range
+// is clamped to the last slot, which is never read back.
+__device__ __forceinline__ uint32_t tile_slot(int row, uint32_t last_slot) {
+  const uint32_t r = static_cast<uint32_t>(row);
+  return r < last_slot ? r : last_slot;
+}
+
+// Exclusive block-wide scan of two counters; part[] holds 2*WAVES words.
+template <int WAVES>
+__device__ __forceinline__ void block_exclusive_scan2(uint32_t a, uint32_t b, uint32_t& ea, uint32_t& eb,
+                                                      uint32_t& ta, uint32_t& tb, uint32_t* part) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  const int ia = wave_inclusive_scan(static_cast<int>(a));
+  const int ib = wave_inclusive_scan(static_cast<int>(b));
+  if (lane == kWave - 1) {
+    part[wv] = static_cast<uint32_t>(ia);
+    part[WAVES + wv] = static_cast<uint32_t>(ib);
+  }
+  __syncthreads();
+  uint32_t oa = 0, ob = 0, sa = 0, sb = 0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    const uint32_t pa = part[w], pb = part[WAVES + w];
+    if (w < wv) {
+      oa += pa;
+      ob += pb;
+    }
+    sa += pa;
+    sb += pb;
+  }
+  ea = oa + static_cast<uint32_t>(ia) - a;
+  eb = ob + static_cast<uint32_t>(ib) - b;
+  ta = sa;
+  tb = sb;
+  __syncthreads();
+}
+
+struct KernelArgs {
+  const uint32_t* gptr;
+  const uint4* values;          // 8 fp16 per uint4
+  const uint32_t* runs;
+  const unsigned short* x;      // fp16 bits
+  unsigned short* y;            // fp16 bits
+  float* ws;                    // [M] fp32 partials
+  uint32_t* counters;           // [T]
+  float tau;
+  int M, K, R, Kc, KC, tile_slots;
+  int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS
+};
+
+template <int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
+  constexpr int NT = WAVES * kWave;
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* tile = reinterpret_cast<float*>(smem);
+  SegInfo* seg = reinterpret_cast<SegInfo*>(smem + p.seg_off);
+  int* scr_all = reinterpret_cast<int*>(smem + p.scr_off);
+  uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 2*WAVES
+  int* wfirst = reinterpret_cast<int*>(part + 2 * WAVES);             // WAVES+1
+  int* last_flag = wfirst + WAVES + 1;                                // 1
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int t = blockIdx.x / p.KC, c = blockIdx.x - t * p.KC;
+  const int row0 = t * p.R;
+  const int rows = min(p.R, p.M - row0);
+  const uint32_t last_slot = static_cast<uint32_t>(p.tile_slots - 1);
+
+  for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0.f;
+  scr_all[tid] = 0;
+
+  // ---- selection of this slice's active, non-empty columns ----------------
+  const int k0 = c * p.Kc;
+  const int kn = min(p.Kc, p.K - k0);
+  const uint32_t* gp = p.gptr + static_cast<size_t>(t) * p.K + k0;
+  uint32_t n_seg = 0, n_grp = 0;
+  for (int it = 0; it < kn; it += NT) {
+    const int kk = it + tid;
+    uint32_t g0 = 0, g1 = 0;
+    float xv = 0.f;
+    bool keep = false;
+    if (kk < kn) {
+      xv = half_bits_to_float(p.x[k0 + kk]);
+      g0 = gp[kk];
+      g1 = gp[kk + 1];
+      keep = (fabsf(xv) > p.tau) && (g1 > g0);
+    }
+    const uint32_t cnt = keep ? g1 - g0 : 0u;
+    uint32_t en, eg, tn, tg;
+    block_exclusive_scan2<WAVES>(keep ? 1u : 0u, cnt, en, eg, tn, tg, part);
+    if (keep) seg[n_seg + en] = SegInfo{g0, n_grp + eg, cnt, xv};
+    n_seg += tn;
+    n_grp += tg;
+  }
+  __syncthreads();
+
+  // ---- cut the flat group sequence into one range per wavefront -----------
+  // segment i goes to wavefront floor(off_i * WAVES / n_grp); wfirst[w] is the
+  // first segment of wavefront w, wfirst[WAVES] = n_seg.
+  for (int i = tid; i < static_cast<int>(n_seg); i += NT) {
+    const int wi = static_cast<int>((static_cast<uint64_t>(seg[i].off) * WAVES) / n_grp);
+    const int wp = i == 0 ? -1 : static_cast<int>((static_cast<uint64_t>(seg[i - 1].off) * WAVES) / n_grp);
+    for (int w = wp + 1; w <= wi; ++w) wfirst[w] = i;
+    if (i == static_cast<int>(n_seg) - 1)
+      for (int w = wi + 1; w <= WAVES; ++w) wfirst[w] = static_cast<int>(n_seg);
+  }
+  if (n_seg == 0 && tid <= WAVES) wfirst[tid] = 0;
+  __syncthreads();
+
+  // ---- per-wavefront walk over 64-group passes ----------------------------
+  const int i_begin = wfirst[wv], i_end = wfirst[wv + 1];
+  if (i_begin < i_end) {
+    int* scr = scr_all + wv * kWave;
+    uint32_t pb = seg[i_begin].off;
+    const uint32_t pe = i_end < static_cast<int>(n_seg) ? seg[i_end].off : n_grp;
+    int icur = i_begin;   // segment holding flat group pb
+    int carry = 0;        // its sum of (run + 1) over groups before pb
+    while (pb < pe) {
+      // heads of the segments that start inside (pb, pb + 64): tag their lane
+      const int j = icur + lane;
+      if (lane > 0 && j < i_end) {
+        const uint32_t o = seg[j].off;
+        if (o < pb + kWave) scr[o - pb] = static_cast<int>(pb + 1u);
+      }
+      wave_lds_sync();
+      const bool head = lane > 0 && scr[lane] == static_cast<int>(pb + 1u);
+      const uint64_t hm = __ballot(head);
+      const int sid = icur + static_cast<int>(lanes_below(hm)) + (head ? 1 : 0);
+      const SegInfo si = seg[sid];
+
+      const uint32_t f = pb + static_cast<uint32_t>(lane);
+      const bool live = f < pe;
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      uint32_t rw = 0u;
+      if (live) {
+        const uint32_t gi = si.gstart + (f - si.off);
+        v = p.values[gi];
+        rw = p.runs[gi];
+      }
+      // byte k of O: inclusive prefix of (run + 1) through entry 2k+1;
+      // byte k of E: the same through entry 2k.
+      const uint32_t r_even = rw & 0x0F0F0F0Fu;
+      const uint32_t r_odd = (rw >> 4) & 0x0F0F0F0Fu;
+      const uint32_t O = (r_even + r_odd + 0x02020202u) * 0x01010101u;
+      const uint32_t E = O - r_odd - 0x01010101u;
+      const int S = live ? static_cast<int>(O >> 24) : 0;   // lane total
+      const int incl = wave_inclusive_scan(S);
+      const int excl = incl - S;
+      const int h = static_cast<int>(si.off) - static_cast<int>(pb);   // head lane of my segment
+      const int eh = __builtin_amdgcn_ds_bpermute((h > 0 ? h : 0) << 2, excl);
+      const int rel = excl - eh + (h < 0 ? carry : 0);                 // segment-relative
+      if (live) {
+        const float xv = si.xv;
+        const int base = rel - 1;   // row of entry j = base + prefix_j
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int re = base + static_cast<int>((E >> (8 * q)) & 0xFFu);
+          const int ro = base + static_cast<int>((O >> (8 * q)) & 0xFFu);
+          atomicAdd(&tile[tile_slot(re, last_slot)], half_bits_to_float(w4[q] & 0xFFFFu) * xv);
+          atomicAdd(&tile[tile_slot(ro, last_slot)], half_bits_to_float(w4[q] >> 16) * xv);
+        }
+      }
+      // the segment that holds the next pass's first group, and its carry
+      const int sid63 = __builtin_amdgcn_readlane(sid, kWave - 1);
+      const uint32_t end63 = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(si.off + si.cnt), kWave - 1));
+      const int carry63 = __builtin_amdgcn_readlane(rel + S, kWave - 1);
+      const uint32_t pn = pb + kWave;
+      if (end63 > pn) {
+        icur = sid63;
+        carry = carry63;
+      } else {
+        icur = sid63 + 1;
+        carry = 0;
+      }
+      pb = pn;
+    }
+  }
+  __syncthreads();
+
+  // ---- merge --------------------------------------------------------------
+  if (p.KC == 1) {
+    for (int r = tid; r < rows; r += NT) p.y[row0 + r] = float_to_half_bits(tile[r]);
+    return;
+  }
+  float* wsr = p.ws + row0;
+  for (int r = tid; r < rows; r += NT) {
+    const float v = tile[r];
+    if (v != 0.f) unsafeAtomicAdd(wsr + r, v);
+  }
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t old = atomicAdd(p.counters + t, 1u);
+    *last_flag = old == static_cast<uint32_t>(p.KC - 1);
+  }
+  __syncthreads();
+  if (*last_flag) {
+    __threadfence();
+    for (int r = tid; r < rows; r += NT) {
+      const float v = __hip_atomic_load(wsr + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      p.y[row0 + r] = float_to_half_bits(v);
+      __hip_atomic_store(wsr + r, 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (tid == 0) __hip_atomic_store(p.counters + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Global selection: one workgroup of 1024 lanes walks x in 1024-wide steps;
+// ballot + mbcnt give each active lane its rank, wave totals are combined in
+// LDS, and indices are written in ascending order.
+__global__ __launch_bounds__(1024) void select_kernel(const unsigned short* __restrict__ x, int K, float tau,
+                                                      int32_t* __restrict__ idx, int32_t* __restrict__ count) {
+  constexpr int NW = 1024 / kWave;
+  __shared__ uint32_t wsum[NW];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  uint32_t base = 0;
+  for (int it = 0; it < K; it += 1024) {
+    const int k = it + tid;
+    const bool act = k < K && fabsf(half_bits_to_float(x[k])) > tau;
+    const uint64_t m = __ballot(act);
+    const uint32_t rank = lanes_below(m);
+    if (lane == 0) wsum[wv] = static_cast<uint32_t>(__popcll(m));
+    __syncthreads();
+    uint32_t off = base, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const uint32_t cw = wsum[w];
+      if (w < wv) off += cw;
+      tot += cw;
+    }
+    if (act) idx[off + rank] = k;
+    base += tot;
+    __syncthreads();
+  }
+  if (tid == 0) *count = static_cast<int32_t>(base);
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Plan {
+  int waves = 4, Kc = 0, KC = 0, T = 0, tile_slots = 0;
+  int seg_off = 0, scr_off = 0, misc_off = 0;
+  int64_t blocks = 0;
+  size_t lds = 0;
+};
+
+bool misaligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
+
+celty_status check_header(const celty_rlc_csc* W) {
+  if (!W) return CELTY_EINVAL;
+  if (W->version != CELTY_FORMAT_VERSION || W->run_bits != CELTY_RUN_BITS) return CELTY_EINVAL;
+  if (W->M < 1 || W->K < 1 || W->R < 1) return CELTY_EINVAL;
+  if (W->T != static_cast<int32_t>((static_cast<int64_t>(W->M) + W->R - 1) / W->R)) return CELTY_EINVAL;
+  if (W->n_groups < 0 || W->n_groups > static_cast<int64_t>(UINT32_MAX)) return CELTY_EINVAL;
+  if (!W->gptr || misaligned(W->gptr, 4)) return CELTY_EINVAL;
+  if (W->n_groups > 0 && (!W->values || !W->runs)) return CELTY_EINVAL;
+  if (misaligned(W->values, 16) || misaligned(W->runs, 4)) return CELTY_EINVAL;
+  return CELTY_OK;
+}
+
+celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl) {
+  if (celty_status st = check_header(W)) return st;
+  pl.T = W->T;
+  pl.waves = (cfg && cfg->waves_per_block) ? cfg->waves_per_block : 4;
+  if (pl.waves != 2 && pl.waves != 4 && pl.waves != 8 && pl.waves != 16) return CELTY_EINVAL;
+  int Kc = cfg ? cfg->cols_per_block : 0;
+  if (Kc == 0) {
+    // aim at ~2048 workgroups (8 per CU) with slices of 64..1024 columns
+    const int64_t want = (2048 + W->T - 1) / W->T;
+    int64_t kc = (W->K + want - 1) / want;
+    kc = (kc + 63) / 64 * 64;
+    if (kc < 64) kc = 64;
+    if (kc > 1024) kc = 1024;
+    Kc = static_cast<int>(kc);
+  }
+  if (Kc < 1 || Kc > 4096) return CELTY_EINVAL;
+  if (Kc > W->K) Kc = W->K;
+  pl.Kc = Kc;
+  pl.KC = (W->K + Kc - 1) / Kc;
+  pl.tile_slots = W->R + 8;
+  size_t off = align_up(static_cast<size_t>(pl.tile_slots) * 4, 16);
+  pl.seg_off = static_cast<int>(off);
+  off += static_cast<size_t>(Kc) * sizeof(SegInfo);
+  pl.scr_off = static_cast<int>(off);
+  off += static_cast<size_t>(pl.waves) * kWave * 4;
+  pl.misc_off = static_cast<int>(off);
+  off += static_cast<size_t>(3 * pl.waves + 2) * 4;
+  pl.lds = align_up(off, 16);
+  if (pl.lds > static_cast<size_t>(kMaxLds)) return CELTY_EINVAL;
+  pl.blocks = static_cast<int64_t>(W->T) * pl.KC;
+  if (pl.blocks > 0x7FFFFFFF) return CELTY_EINVAL;
+  return CELTY_OK;
+}
+
+template <int WAVES>
+celty_status launch(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
+  static bool attr_set = false;
+  if (pl.lds > 64 * 1024 && !attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&spmspv_kernel<WAVES>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds) != hipSuccess)
+      return CELTY_EHIP;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(spmspv_kernel<WAVES>, dim3(static_cast<unsigned>(pl.blocks)), dim3(WAVES * kWave),
+                     pl.lds, stream, a);
+  return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
+}
+
+}  // namespace
+
+extern "C" size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R) {
+  (void)K;
+  if (M < 1 || R < 1) return 0;
+  const int64_t T = (static_cast<int64_t>(M) + R - 1) / R;
+  return align_up(static_cast<size_t>(M) * 4, 256) + align_up(static_cast<size_t>(T) * 4, 256);
+}
+
+extern "C" celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace || workspace_bytes == 0) return CELTY_EINVAL;
+  return hipMemsetAsync(workspace, 0, workspace_bytes, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? CELTY_OK
+             : CELTY_EHIP;
+}
+
+extern "C" celty_status celty_spmspv_plan(const celty_rlc_csc* W, const celty_launch* launch_cfg,
+                                          celty_launch* resolved, int64_t* n_blocks, int64_t* lds_bytes) {
+  if (!resolved) return CELTY_EINVAL;
+  Plan pl;
+  if (celty_status st = make_plan(W, launch_cfg, pl)) return st;
+  resolved->cols_per_block = pl.Kc;
+  resolved->waves_per_block = pl.waves;
+  if (n_blocks) *n_blocks = pl.blocks;
+  if (lds_bytes) *lds_bytes = static_cast<int64_t>(pl.lds);
+  return CELTY_OK;
+}
+
+extern "C" celty_status celty_spmspv_ex(const celty_rlc_csc* W, const void* x, float tau, void* y,
+                                        void* workspace, size_t workspace_bytes, const celty_launch* launch_cfg,
+                                        void* stream) {
+  Plan pl;
+  if (celty_status st = make_plan(W, launch_cfg, pl)) return st;
+  if (!x || !y || misaligned(x, 2) || misaligned(y, 2) || std::isnan(tau)) return CELTY_EINVAL;
+  const uintptr_t xb = reinterpret_cast<uintptr_t>(x), yb = reinterpret_cast<uintptr_t>(y);
+  if (xb < yb + 2u * static_cast<uintptr_t>(W->M) && yb < xb + 2u * static_cast<uintptr_t>(W->K))
+    return CELTY_EINVAL;   // x and y overlap
+  const size_t need = celty_spmspv_workspace_bytes(W->M, W->K, W->R);
+  if (!workspace || misaligned(workspace, 256) || workspace_bytes < need) return CELTY_EINVAL;
+
+  KernelArgs a;
+  a.gptr = W->gptr;
+  a.values = reinterpret_cast<const uint4*>(W->values);
+  a.runs = W->runs;
+  a.x = static_cast<const unsigned short*>(x);
+  a.y = static_cast<unsigned short*>(y);
+  a.ws = static_cast<float*>(workspace);
+  a.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + align_up(static_cast<size_t>(W->M) * 4, 256));
+  a.tau = tau;
+  a.M = W->M;
+  a.K = W->K;
+  a.R = W->R;
+  a.Kc = pl.Kc;
+  a.KC = pl.KC;
+  a.tile_slots = pl.tile_slots;
+  a.seg_off = pl.seg_off;
+  a.scr_off = pl.scr_off;
+  a.misc_off = pl.misc_off;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (pl.waves) {
+    case 2: return launch<2>(pl, a, s);
+    case 4: return launch<4>(pl, a, s);
+    case 8: return launch<8>(pl, a, s);
+    case 16: return launch<16>(pl, a, s);
+    default: return CELTY_EINVAL;
+  }
+}
+
+extern "C" celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  return celty_spmspv_ex(W, x, tau, y, workspace, workspace_bytes, nullptr, stream);
+}
+
+extern "C" celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int32_t* count,
+                                     void* stream) {
+  if (!x || !idx || !count || K < 1 || std::isnan(tau)) return CELTY_EINVAL;
+  if (misaligned(x, 2) || misaligned(idx, 4) || misaligned(count, 4)) return CELTY_EINVAL;
+  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(1024), 0, static_cast<hipStream_t>(stream),
+                     static_cast<const unsigned short*>(x), K, tau, idx, count);
+  return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
+}
+
+extern "C" const char* celty_status_string(celty_status status) {
+  switch (status) {
+    case CELTY_OK: return "CELTY_OK: success";
+    case CELTY_EINVAL: return "CELTY_EINVAL: invalid argument";
+    case CELTY_ENOMEM: return "CELTY_ENOMEM: host scratch or worker threads unavailable";
+    case CELTY_EOVERFLOW: return "CELTY_EOVERFLOW: group count exceeds uint32";
+    case CELTY_EFORMAT: return "CELTY_EFORMAT: malformed RLC-CSC stream";
+    case CELTY_EHIP: return "CELTY_EHIP: HIP runtime error";
+  }
+  return "unknown celty_status";
+}

@@ -1,0 +1,204 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects bad
+arguments with the documented status before touching the device.
+
+The rejection checks pass fake (never dereferenced) device addresses; they run
+only where no GPU is visible, so a validation bug can never launch a kernel on
+garbage pointers.
+"""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2608_01536_amd as celty
+from paper_2608_01536_amd import (CELTY_EFORMAT, CELTY_EINVAL, CELTY_OK, celty_launch, celty_rlc_csc)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "celty.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^[A-Za-z_][\w\s\*]*?\b(celty_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for want in ("celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv",
+                 "celty_spmspv_ex", "celty_spmspv_plan", "celty_spmspv_workspace_bytes",
+                 "celty_spmspv_workspace_init", "celty_status_string"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(celty._LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", celty._LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (celty_\w+)", out))
+    assert set(_declared_functions()) <= exported
+
+
+def test_status_strings():
+    for st in range(6):
+        assert celty.celty_status_string(st).startswith("CELTY_")
+    assert "unknown" in celty.celty_status_string(99)
+
+
+def test_workspace_bytes():
+    assert celty.celty_spmspv_workspace_bytes(4096, 4096, 256) == 4096 * 4 + 256
+    assert celty.celty_spmspv_workspace_bytes(1000, 7, 300) == 4096 + 256
+    assert celty.celty_spmspv_workspace_bytes(0, 1, 1) == 0
+
+
+# --------------------------------------------------------------------------
+# encoder / decoder error paths (pure host)
+# --------------------------------------------------------------------------
+def test_encode_plan_rejects_bad_arguments():
+    W = np.ones((4, 5), dtype=np.float16).view(np.uint16)
+    g, n, p = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    f = celty._encode_plan
+    ok = f(W.ctypes.data, 5, None, 0, 4, 5, 2, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p))
+    assert ok == CELTY_OK and n.value == 20 and p.value == 0 and g.value == 10
+    assert f(None, 5, None, 0, 4, 5, 2, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
+    assert f(W.ctypes.data, 4, None, 0, 4, 5, 2, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
+    assert f(W.ctypes.data, 5, W.ctypes.data, 3, 4, 5, 2, ctypes.byref(g), ctypes.byref(n),
+             ctypes.byref(p)) == CELTY_EINVAL
+    for M, K, R in ((0, 5, 2), (4, 0, 2), (4, 5, 0)):
+        assert f(W.ctypes.data, 5, None, 0, M, K, R, ctypes.byref(g), ctypes.byref(n),
+                 ctypes.byref(p)) == CELTY_EINVAL
+    assert f(W.ctypes.data, 5, None, 0, 4, 5, 2, None, ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
+
+
+def test_encode_rejects_bad_arguments():
+    W = np.ones((4, 5), dtype=np.float16).view(np.uint16)
+    gptr = celty._aligned_empty(3 * 5 + 1, np.uint32)
+    vals = celty._aligned_empty(8 * 20, np.uint16)
+    runs = celty._aligned_empty(20, np.uint32)
+    d = celty_rlc_csc()
+    f = celty._encode
+    args = [W.ctypes.data, 5, None, 0, 4, 5, 2, gptr.ctypes.data, vals.ctypes.data, runs.ctypes.data]
+    assert f(*args, 10, ctypes.byref(d), 1) == CELTY_OK
+    assert f(*args, 11, ctypes.byref(d), 1) == CELTY_EINVAL          # n_groups mismatch
+    assert f(*args, 10, ctypes.byref(d), -1) == CELTY_EINVAL         # n_threads
+    bad = list(args)
+    bad[8] = vals.ctypes.data + 2                                    # values not 16-byte aligned
+    assert f(*bad, 10, ctypes.byref(d), 1) == CELTY_EINVAL
+    assert f(*args, 10, None, 1) == CELTY_EINVAL
+
+
+def test_decode_rejects_corrupt_streams():
+    rng = np.random.default_rng(0)
+    W = (rng.standard_normal((40, 6)) * 0.02).astype(np.float16)
+    enc = celty.celty_encode(W, (rng.random((40, 6)) < 0.5).astype(np.uint8), 16)
+    d = enc.desc()
+    out = np.empty((40, 6), np.uint16)
+    m = np.empty((40, 6), np.uint8)
+    assert celty._decode(ctypes.byref(d), out.ctypes.data, m.ctypes.data) == CELTY_OK
+    g = enc.gptr.copy()
+    g[3], g[4] = g[4] + 1, g[3]                                      # non-monotone
+    d2 = enc.desc()
+    d2.gptr = g.ctypes.data
+    assert celty._decode(ctypes.byref(d2), out.ctypes.data, m.ctypes.data) == CELTY_EFORMAT
+    d3 = enc.desc()
+    d3.n_nnz += 1                                                    # header disagrees
+    assert celty._decode(ctypes.byref(d3), out.ctypes.data, m.ctypes.data) == CELTY_EFORMAT
+    d4 = enc.desc()
+    d4.T += 1                                                        # inconsistent header
+    assert celty._decode(ctypes.byref(d4), out.ctypes.data, m.ctypes.data) == CELTY_EINVAL
+    d5 = enc.desc()
+    d5.version = 2
+    assert celty._decode(ctypes.byref(d5), out.ctypes.data, m.ctypes.data) == CELTY_EINVAL
+
+
+# --------------------------------------------------------------------------
+# device entry points: validation before any launch (no GPU visible only)
+# --------------------------------------------------------------------------
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+host_only = pytest.mark.skipif(_gpu_visible(), reason="fake device addresses are only used without a GPU")
+
+FAKE = 0x7F0000000000   # never dereferenced: every call below fails validation first
+
+
+def _desc(M=4096, K=4096, R=256, G=1000):
+    T = -(-M // R)
+    return celty_rlc_csc(1, M, K, R, T, 4, G, 8 * G, 7 * G, G, FAKE, FAKE + 0x10000, FAKE + 0x20000)
+
+
+@host_only
+def test_spmspv_plan_is_host_only():
+    d = _desc()
+    out, nb, lds = celty_launch(), ctypes.c_int64(), ctypes.c_int64()
+    assert celty._plan(ctypes.byref(d), None, ctypes.byref(out), ctypes.byref(nb), ctypes.byref(lds)) == CELTY_OK
+    assert out.waves_per_block in (2, 4, 8, 16) and 1 <= out.cols_per_block <= 4096
+    assert nb.value == d.T * (-(-d.K // out.cols_per_block))
+    assert 0 < lds.value <= 160 * 1024
+    bad = celty_launch(64, 3)
+    assert celty._plan(ctypes.byref(d), ctypes.byref(bad), ctypes.byref(out), None, None) == CELTY_EINVAL
+    bad = celty_launch(5000, 4)
+    assert celty._plan(ctypes.byref(d), ctypes.byref(bad), ctypes.byref(out), None, None) == CELTY_EINVAL
+    big = _desc(M=100000, K=64, R=60000)                             # tile does not fit in LDS
+    assert celty._plan(ctypes.byref(big), None, ctypes.byref(out), None, None) == CELTY_EINVAL
+
+
+@host_only
+@pytest.mark.parametrize("case", ["null_desc", "version", "run_bits", "T", "values_align", "runs_align",
+                                  "null_x", "nan_tau", "x_align", "overlap", "short_ws", "null_ws",
+                                  "ws_align", "waves"])
+def test_spmspv_rejects_bad_arguments(case):
+    d = _desc()
+    x, y, ws = FAKE + 0x100000, FAKE + 0x200000, FAKE + 0x300000
+    tau = 0.5
+    nws = celty.celty_spmspv_workspace_bytes(4096, 4096, 256)
+    launch = None
+    if case == "version":
+        d.version = 2
+    elif case == "run_bits":
+        d.run_bits = 3
+    elif case == "T":
+        d.T += 1
+    elif case == "values_align":
+        d.values += 8
+    elif case == "runs_align":
+        d.runs += 2
+    elif case == "null_x":
+        x = None
+    elif case == "nan_tau":
+        tau = math.nan
+    elif case == "x_align":
+        x += 1
+    elif case == "overlap":
+        y = x + 100
+    elif case == "short_ws":
+        nws -= 1
+    elif case == "null_ws":
+        ws = None
+    elif case == "ws_align":
+        ws += 16
+    elif case == "waves":
+        launch = celty_launch(64, 5)
+    pd = None if case == "null_desc" else ctypes.byref(d)
+    st = celty._spmspv_ex(pd, x, tau, y, ws, nws, None if launch is None else ctypes.byref(launch), None)
+    assert st == CELTY_EINVAL
+
+
+@host_only
+def test_select_rejects_bad_arguments():
+    f = celty._select
+    assert f(None, 10, 0.5, FAKE, FAKE + 64, None) == CELTY_EINVAL
+    assert f(FAKE, 0, 0.5, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
+    assert f(FAKE, 10, math.nan, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
+    assert f(FAKE, 10, 0.5, FAKE + 66, FAKE + 128, None) == CELTY_EINVAL

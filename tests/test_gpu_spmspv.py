@@ -1,0 +1,243 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+* selection: the active index list is bit-exact;
+* y: max|y - y*| / (max|y*| + 1e-6) <= 2e-3 with y* the fp64 definition;
+* exact special cases (single-term rows): one-hot x, identity pattern,
+  all-inactive x (every row +0), empty matrix;
+* edge shapes: M < R, M % R != 0, K = 1, K not a multiple of 64, R = 1;
+* every launch shape gives the same answer within tolerance;
+* the workspace is left zero-filled by every call; y is fully overwritten;
+* full-size runs of all five benchmark configurations in the launch shape
+  the benchmark uses.
+"""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import spmspv as ref
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch, torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def celty():
+    import paper_2608_01536_amd as c
+    return c
+
+
+def _note(msg):
+    print(msg, flush=True)
+
+
+def _run(celty, torch_dev, W, mask, x, tau, R, launch=None, check_ws=True, enc=None):
+    torch, dev = torch_dev
+    if enc is None:
+        enc = celty.celty_encode(W, mask, R)
+    Wd = enc.to_device(dev)
+    xt = torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(dev)
+    y = torch.full((W.shape[0],), 0x7C01, dtype=torch.int16, device=dev)   # NaN bits
+    ws = celty.new_workspace(Wd, dev)
+    if launch is None:
+        celty.celty_spmspv(Wd, xt, tau, y, ws)
+    else:
+        celty.celty_spmspv_ex(Wd, xt, tau, y, ws, launch)
+    torch.cuda.synchronize()
+    if check_ws:
+        assert int(ws.count_nonzero()) == 0, "workspace not left zero-filled"
+    return y.cpu().numpy().view(np.float16)
+
+
+def _check(y, W, mask, x, tau):
+    want = ref.spmspv_dense_fp64(W, mask, x, tau)
+    err = ref.rel_error(y.astype(np.float64), want)
+    assert np.all(np.isfinite(y)), "y has non-finite rows"
+    assert err <= TOL, err
+    return err
+
+
+# --------------------------------------------------------------------------
+# selection
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("K", [1, 63, 64, 65, 1000, 1024, 1025, 4096, 11008, 28672])
+@pytest.mark.parametrize("mode", ["median", "neg", "zero", "max", "nan"])
+def test_select_bit_exact(celty, torch_dev, K, mode):
+    torch, dev = torch_dev
+    _note(f"select K={K} mode={mode}")
+    rng = np.random.default_rng(K)
+    x = rng.laplace(size=K).astype(np.float16)
+    x[rng.random(K) < 0.1] = 0
+    if mode == "nan":
+        x[rng.random(K) < 0.05] = np.nan
+    tau = {"median": workloads.tau_for_sparsity(x, 50), "neg": -1.0, "zero": 0.0,
+           "max": float(np.nanmax(np.abs(x.astype(np.float32)))), "nan": 0.3}[mode]
+    xt = torch.from_numpy(x.view(np.int16)).to(dev)
+    idx = torch.full((K,), -7, dtype=torch.int32, device=dev)
+    cnt = torch.zeros(1, dtype=torch.int32, device=dev)
+    celty.celty_select(xt, tau, idx, cnt)
+    torch.cuda.synchronize()
+    want = ref.select_active(x, tau)
+    n = int(cnt.item())
+    assert n == want.size
+    assert np.array_equal(idx[:n].cpu().numpy(), want)
+
+
+# --------------------------------------------------------------------------
+# small fuzz and edge shapes
+# --------------------------------------------------------------------------
+FUZZ = [(1, 1, 1), (1, 5, 8), (5, 1, 8), (3, 200, 1), (100, 100, 16), (257, 129, 256), (255, 1000, 256),
+        (700, 513, 256), (1024, 64, 1024), (1500, 300, 512), (2049, 777, 128), (64, 4100, 64)]
+
+
+@pytest.mark.parametrize("M,K,R", FUZZ)
+@pytest.mark.parametrize("ws,as_", [(0, 0), (50, 50), (90, 30), (30, 90)])
+def test_spmspv_fuzz(celty, torch_dev, M, K, R, ws, as_):
+    _note(f"fuzz M={M} K={K} R={R} ws={ws} as={as_}")
+    p = workloads.random_small(M * 13 + K * 7 + R + ws, M, K, ws=ws, as_=as_, zero_weights=3)
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, R)
+    _check(y, p.W, p.mask, p.x, p.tau)
+
+
+@pytest.mark.parametrize("launch", [(1, 2), (17, 4), (64, 2), (64, 4), (128, 8), (256, 16), (1000, 4),
+                                    (4096, 4), (4096, 16)])
+def test_launch_shapes_agree(celty, torch_dev, launch):
+    _note(f"launch shape {launch}")
+    p = workloads.random_small(77, 3000, 2500, ws=60, as_=50)
+    enc = celty.celty_encode(p.W, p.mask, 256)
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, 256, launch=launch, enc=enc)
+    _check(y, p.W, p.mask, p.x, p.tau)
+
+
+def test_one_hot_returns_column_exactly(celty, torch_dev):
+    rng = np.random.default_rng(3)
+    M, K = 3000, 700
+    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float16)
+    mask = (rng.random((M, K)) < 0.5).astype(np.uint8)
+    enc = celty.celty_encode(W, mask, 256)
+    for k in (0, 1, 350, K - 1):
+        _note(f"one-hot k={k}")
+        x = np.zeros(K, dtype=np.float16)
+        x[k] = 1
+        y = _run(celty, torch_dev, W, mask, x, 0.5, 256, enc=enc)
+        want = np.where(mask[:, k] != 0, W[:, k], np.float16(0)).astype(np.float16)
+        assert np.array_equal(y.view(np.uint16), want.view(np.uint16))
+
+
+def test_identity_pattern_returns_active_x(celty, torch_dev):
+    K = 2000
+    I = np.eye(K, dtype=np.float16)
+    x = np.random.default_rng(4).laplace(size=K).astype(np.float16)
+    tau = 0.8
+    _note("identity pattern")
+    y = _run(celty, torch_dev, I, None, x, tau, 128)
+    want = np.where(np.abs(x.astype(np.float32)) > tau, x, np.float16(0)).astype(np.float16)
+    assert np.array_equal(y.view(np.uint16), want.view(np.uint16))
+
+
+def test_all_inactive_gives_positive_zero(celty, torch_dev):
+    p = workloads.random_small(9, 1000, 900, ws=50, as_=50)
+    tau = float(np.max(np.abs(p.x.astype(np.float32))))
+    _note("all inactive")
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, tau, 256)
+    assert np.all(y.view(np.uint16) == 0)
+
+
+def test_empty_matrix(celty, torch_dev):
+    W = np.zeros((300, 200), dtype=np.float16)
+    x = np.ones(200, dtype=np.float16)
+    _note("empty matrix")
+    y = _run(celty, torch_dev, W, None, x, -1.0, 64)
+    assert np.all(y.view(np.uint16) == 0)
+
+
+def test_weight_only_full_mask_is_dense_gemv(celty, torch_dev):
+    rng = np.random.default_rng(12)
+    M, K = 1024, 768
+    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float16)
+    x = rng.standard_normal(K).astype(np.float16)
+    _note("tau<0 full mask")
+    y = _run(celty, torch_dev, W, None, x, -1.0, 256)
+    want = W.astype(np.float64) @ x.astype(np.float64)
+    assert ref.rel_error(y.astype(np.float64), want) <= TOL
+
+
+def test_repeated_calls_share_a_workspace(celty, torch_dev):
+    torch, dev = torch_dev
+    p = workloads.random_small(10, 2500, 3000, ws=50, as_=50)
+    enc = celty.celty_encode(p.W, p.mask, 256)
+    Wd = enc.to_device(dev)
+    ws = celty.new_workspace(Wd, dev)
+    want = ref.spmspv_dense_fp64(p.W, p.mask, p.x, p.tau)
+    xt = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    outs = []
+    _note("repeated calls")
+    for i in range(5):
+        y = torch.empty(p.W.shape[0], dtype=torch.int16, device=dev)
+        celty.celty_spmspv(Wd, xt, p.tau, y, ws)
+        outs.append(y)
+    torch.cuda.synchronize()
+    assert int(ws.count_nonzero()) == 0
+    for y in outs:
+        assert ref.rel_error(y.cpu().numpy().view(np.float16).astype(np.float64), want) <= TOL
+
+
+# --------------------------------------------------------------------------
+# full-size benchmark configurations
+# --------------------------------------------------------------------------
+def _full(celty, torch_dev, p, label):
+    from paper_2608_01536_amd import default_tile_rows
+    R = default_tile_rows(p.W.shape[0], p.W.shape[1])
+    _note(f"full {label} M={p.W.shape[0]} K={p.W.shape[1]} R={R}")
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, R)
+    return _check(y, p.W, p.mask, p.x, p.tau)
+
+
+def test_config1(celty, torch_dev):
+    c = workloads.CONFIGS[1]
+    p = workloads.make_problem(1, 4096, 4096, c["ws"], c["as_"], c["xdist"], seed=0, proj=7)
+    _full(celty, torch_dev, p, "config1")
+
+
+@pytest.mark.parametrize("ws", [30, 50, 70])
+@pytest.mark.parametrize("as_", [30, 50, 70])
+def test_config2_sweep_seed0(celty, torch_dev, ws, as_):
+    p = workloads.make_problem(2, 4096, 4096, ws, as_, "laplace", seed=0, proj=7)
+    _full(celty, torch_dev, p, f"config2 ws{ws} as{as_}")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3, 4])
+def test_config2_headline_seeds(celty, torch_dev, seed):
+    p = workloads.headline_problem(seed)
+    _full(celty, torch_dev, p, f"headline seed{seed}")
+
+
+def test_config3_layer(celty, torch_dev):
+    for p in workloads.layer_problems(3, 0, 0):
+        _full(celty, torch_dev, p, f"config3 {p.meta['proj_name']}")
+
+
+@pytest.mark.parametrize("layer", [0, 39])
+def test_config4_layer(celty, torch_dev, layer):
+    for p in workloads.layer_problems(4, 0, layer):
+        _full(celty, torch_dev, p, f"config4 layer{layer} {p.meta['proj_name']}")
+
+
+@pytest.mark.parametrize("as_", [40, 60, 80])
+def test_config5_projections(celty, torch_dev, as_):
+    # one of each distinct 70B shape: q (8192^2), k (1024x8192), gate (28672x8192), down (8192x28672)
+    c = workloads.CONFIGS[5]
+    for name in ("q", "k", "gate", "down"):
+        proj = next(pp for pp in c["layers"] if pp.name == name)
+        x = workloads.shared_x(5, 0, 0, proj.x_group, proj.K, c["xdist"])
+        p = workloads.make_problem(5, proj.M, proj.K, c["ws"], as_, c["xdist"], seed=0, layer=0,
+                                   proj=workloads.PROJ_IDS[name], x=x)
+        _full(celty, torch_dev, p, f"config5 as{as_} {name}")
