@@ -18,6 +18,25 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcelty.so")
 if not os.path.exists(_LIB_PATH):
     raise ImportError(f"{_LIB_PATH} is not built; run `python paper_2608_01536_amd/build_lib.py`")
+
+
+def _share_torch_hip_runtime() -> None:
+    """Make libcelty bind to the HIP runtime torch uses.
+
+    torch ships its own libamdhip64 (same soname as the system one).  Loading
+    it first, by path and globally, makes libcelty's dependency resolve to that
+    copy whatever the import order, so streams and device memory handed over
+    from torch belong to the runtime that launches the kernels."""
+    import importlib.util
+    spec = importlib.util.find_spec("torch")
+    for d in (spec.submodule_search_locations or []) if spec else []:
+        path = os.path.join(d, "lib", "libamdhip64.so")
+        if os.path.exists(path):
+            ctypes.CDLL(path, mode=ctypes.RTLD_GLOBAL)
+            return
+
+
+_share_torch_hip_runtime()
 _lib = ctypes.CDLL(_LIB_PATH)
 
 CELTY_OK, CELTY_EINVAL, CELTY_ENOMEM, CELTY_EOVERFLOW, CELTY_EFORMAT, CELTY_EHIP = range(6)

@@ -202,3 +202,11 @@ def test_select_rejects_bad_arguments():
     assert f(FAKE, 0, 0.5, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
     assert f(FAKE, 10, math.nan, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
     assert f(FAKE, 10, 0.5, FAKE + 66, FAKE + 128, None) == CELTY_EINVAL
+
+
+def test_single_hip_runtime_alongside_torch():
+    """libcelty and torch must share one HIP runtime (torch bundles its own
+    libamdhip64); two runtimes would make torch's streams invalid handles."""
+    import torch  # noqa: F401
+    maps = {l.split()[-1] for l in open("/proc/self/maps") if "libamdhip64" in l}
+    assert len(maps) == 1, maps
