@@ -12,8 +12,8 @@ exceed 1 GiB (beyond the 256 MiB Infinity Cache and the L2s) and the steps
 rotate over them, so every step streams its weights from HBM.
 
 Printed (one JSON line): µs per SpMSpV (value, lower is better), effective
-GB/s on algorithmic bytes, the roofline of the kernel measured with per-launch
-HIP events on the launch stream, the dense fp16 GEMV (torch F.linear, i.e.
+GB/s on algorithmic bytes, the roofline of the kernel (HIP events around a
+graph replay of the K steps on the launch stream), the dense fp16 GEMV (torch F.linear, i.e.
 hipBLASLt/rocBLAS) on the same shape under the same cold protocol, the
 floor of a near-empty kernel, and the CPU oracle timed on a bounded sample.
 """
@@ -77,16 +77,28 @@ def time_loop(torch, fn, steps: int) -> float:
     return s.elapsed_time(e) * 1e3 / steps
 
 
-def time_per_launch(torch, fn, steps: int) -> np.ndarray:
-    """Per-call durations (µs), each call bracketed by its own events."""
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+def time_graph(torch, fn, steps: int, replays: int = 5) -> tuple:
+    """Capture `steps` calls in one HIP graph; return (µs per call of the timed
+    replay, per-replay µs-per-call samples).  Replaying removes host launch
+    overhead, so each call's time is its kernel plus the graph's inter-kernel
+    gap."""
+    g = torch.cuda.CUDAGraph()
     torch.cuda.synchronize()
-    for i in range(steps):
-        ev[i][0].record()
-        fn(i)
-        ev[i][1].record()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            fn(i)
+    g.replay()
     torch.cuda.synchronize()
-    return np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+    samples = []
+    for _ in range(replays):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        g.replay()
+        e.record()
+        torch.cuda.synchronize()
+        samples.append(s.elapsed_time(e) * 1e3 / steps)
+    del g
+    return float(np.median(samples)), samples
 
 
 def cpu_baseline(p, budget_s: float) -> dict:
@@ -159,25 +171,27 @@ def main() -> int:
     ws = celty.new_workspace(base, dev)
     launch = (args.cols, args.waves) if (args.cols or args.waves) else None
     plan = celty.celty_spmspv_plan(base, launch)
-    stream = torch.cuda.current_stream()
-
     def step(i):
-        celty.celty_spmspv_ex(copies[i % ncopies], x, p.tau, y, ws, launch, stream)
+        # stream = None: the binding launches on torch's current stream, which
+        # is the capture stream while a graph is being recorded
+        celty.celty_spmspv_ex(copies[i % ncopies], x, p.tau, y, ws, launch)
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     print(f"[bench] warmup done: {M}x{K} ws{args.ws:g} as{args.as_:g} R={R} copies={ncopies} plan={plan}",
           file=sys.stderr, flush=True)
-    us_step = time_loop(torch, step, args.steps)
-    per_launch = time_per_launch(torch, step, args.steps)
-    us_kernel = float(per_launch.mean())
-    print(f"[bench] timed: {us_step:.2f} us/step, kernel {us_kernel:.2f} us", file=sys.stderr, flush=True)
+    eager_us = time_loop(torch, step, args.steps)
+    # the timed region: K steps captured in one HIP graph and replayed on the
+    # launch stream; one step is exactly one kernel launch
+    us_step, samples = time_graph(torch, lambda i: step(i), args.steps)
+    us_kernel = us_step
+    print(f"[bench] timed: {us_step:.3f} us/step (graph), eager {eager_us:.2f} us/call", file=sys.stderr, flush=True)
 
     # floor: a near-empty kernel (one-element fill) under the same timing
     tiny = torch.zeros(1, device=dev)
     floor_wall = time_loop(torch, lambda i: tiny.fill_(1.0), args.steps)
-    floor_kernel = float(time_per_launch(torch, lambda i: tiny.fill_(1.0), args.steps).mean())
+    floor_kernel, _ = time_graph(torch, lambda i: tiny.fill_(1.0), args.steps)
 
     dense = None
     if not args.no_dense:
@@ -187,9 +201,14 @@ def main() -> int:
         xd = torch.from_numpy(np.where(np.abs(p.x.astype(np.float32)) > p.tau, p.x, np.float16(0))).to(dev)[None]
         for i in range(20):
             F.linear(xd, dcopies[i % nd])
-        dense_us = time_loop(torch, lambda i: F.linear(xd, dcopies[i % nd]), max(200, args.steps // 2))
+        try:
+            dense_us, _ = time_graph(torch, lambda i: F.linear(xd, dcopies[i % nd]), args.steps)
+            dense_mode = "graph"
+        except Exception:
+            dense_us, dense_mode = time_loop(torch, lambda i: F.linear(xd, dcopies[i % nd]), args.steps), "eager"
         dense = {"us": round(dense_us, 3), "GBps": round((2 * M * K + 2 * K + 2 * M) / dense_us / 1e3, 1),
-                 "op": "torch.nn.functional.linear fp16, batch 1 (hipBLASLt/rocBLAS)", "copies": nd}
+                 "op": "torch.nn.functional.linear fp16, batch 1 (hipBLASLt/rocBLAS)", "copies": nd,
+                 "timing": dense_mode}
         del dcopies, Wf
         torch.cuda.empty_cache()
 
@@ -224,10 +243,11 @@ def main() -> int:
         "active_entries": e_a,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
-                     "kernel_us": round(us_kernel, 3), "kernel_us_p10": round(float(np.percentile(per_launch, 10)), 3),
-                     "kernel_us_p90": round(float(np.percentile(per_launch, 90)), 3),
-                     "bytes_per_launch": b_alg},
-        "launch_floor": {"wall_us": round(floor_wall, 3), "kernel_us": round(floor_kernel, 3),
+                     "kernel_us": round(us_kernel, 3), "kernel_us_replays": [round(v, 3) for v in samples],
+                     "bytes_per_launch": b_alg,
+                     "timing": "HIP events around a graph replay of the K steps on the launch stream"},
+        "eager_us_per_call": round(eager_us, 3),
+        "launch_floor": {"graph_us": round(floor_kernel, 3), "eager_us": round(floor_wall, 3),
                          "op": "one-element torch fill kernel"},
         "dense_gemv": dense,
         "speedup_vs_dense": round(dense["us"] / us_step, 3) if dense else None,

@@ -13,8 +13,10 @@
 //     the 8 runs into 8 inclusive prefixes with byte-packed arithmetic,
 //     combines lanes with a wavefront inclusive scan that restarts at segment
 //     heads (Algorithm 1: prefix of runs plus ordinal gives the row), and
-//     adds value * x_k in fp32 into an LDS tile of the R output rows
-//     (Section 3.3: scatter-accumulation in on-chip memory);
+//     adds value * x_k (an exact fp32 product) into an fp64 LDS tile of the R
+//     output rows (Section 3.3: scatter-accumulation in on-chip memory; on
+//     gfx950 the LDS fp64 atomic add is an order of magnitude faster than the
+//     fp32 one, and it only makes the sum more accurate);
 //   * the tile is merged across slices with fp32 atomics into a workspace row
 //     block; the last workgroup of a row tile (counter) writes y in fp16 and
 //     clears its workspace rows and counter for the next call.  With a single
@@ -128,7 +130,7 @@ template <int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   constexpr int NT = WAVES * kWave;
   extern __shared__ __align__(16) unsigned char smem[];
-  float* tile = reinterpret_cast<float*>(smem);
+  double* tile = reinterpret_cast<double*>(smem);
   SegInfo* seg = reinterpret_cast<SegInfo*>(smem + p.seg_off);
   int* scr_all = reinterpret_cast<int*>(smem + p.scr_off);
   uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 2*WAVES
@@ -141,7 +143,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   const int rows = min(p.R, p.M - row0);
   const uint32_t last_slot = static_cast<uint32_t>(p.tile_slots - 1);
 
-  for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0.f;
+  for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0.0;
   scr_all[tid] = 0;
 
   // ---- selection of this slice's active, non-empty columns ----------------
@@ -232,8 +234,9 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
         for (int q = 0; q < 4; ++q) {
           const int re = base + static_cast<int>((E >> (8 * q)) & 0xFFu);
           const int ro = base + static_cast<int>((O >> (8 * q)) & 0xFFu);
-          atomicAdd(&tile[tile_slot(re, last_slot)], half_bits_to_float(w4[q] & 0xFFFFu) * xv);
-          atomicAdd(&tile[tile_slot(ro, last_slot)], half_bits_to_float(w4[q] >> 16) * xv);
+          // the fp32 product of two fp16 values is exact; it is summed in fp64
+          atomicAdd(&tile[tile_slot(re, last_slot)], static_cast<double>(half_bits_to_float(w4[q] & 0xFFFFu) * xv));
+          atomicAdd(&tile[tile_slot(ro, last_slot)], static_cast<double>(half_bits_to_float(w4[q] >> 16) * xv));
         }
       }
       // the segment that holds the next pass's first group, and its carry
@@ -255,15 +258,21 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
 
   // ---- merge --------------------------------------------------------------
   if (p.KC == 1) {
-    for (int r = tid; r < rows; r += NT) p.y[row0 + r] = float_to_half_bits(tile[r]);
+    for (int r = tid; r < rows; r += NT) p.y[row0 + r] = float_to_half_bits(static_cast<float>(tile[r]));
     return;
   }
+  // Returning device-scope atomics are performed at the device's coherence
+  // point before they return; waiting for them (workgroup-scope release) and
+  // then bumping the tile counter orders them before the last workgroup's
+  // device-coherent loads, without writing back or invalidating the L2s.
   float* wsr = p.ws + row0;
+  float sink = 0.f;
   for (int r = tid; r < rows; r += NT) {
-    const float v = tile[r];
-    if (v != 0.f) unsafeAtomicAdd(wsr + r, v);
+    const float v = static_cast<float>(tile[r]);
+    if (v != 0.f) sink += unsafeAtomicAdd(wsr + r, v);
   }
-  __threadfence();
+  asm volatile("" ::"v"(sink));
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __syncthreads();
   if (tid == 0) {
     const uint32_t old = atomicAdd(p.counters + t, 1u);
@@ -271,7 +280,6 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   }
   __syncthreads();
   if (*last_flag) {
-    __threadfence();
     for (int r = tid; r < rows; r += NT) {
       const float v = __hip_atomic_load(wsr + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       p.y[row0 + r] = float_to_half_bits(v);
@@ -357,7 +365,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   pl.Kc = Kc;
   pl.KC = (W->K + Kc - 1) / Kc;
   pl.tile_slots = W->R + 8;
-  size_t off = align_up(static_cast<size_t>(pl.tile_slots) * 4, 16);
+  size_t off = align_up(static_cast<size_t>(pl.tile_slots) * 8, 16);
   pl.seg_off = static_cast<int>(off);
   off += static_cast<size_t>(Kc) * sizeof(SegInfo);
   pl.scr_off = static_cast<int>(off);
