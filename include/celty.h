@@ -9,8 +9,10 @@
  *
  *     y[r] = sum over active k of W[r,k] * x_k,     r = 0 .. M-1,
  *
- * with fp32 products and fp32 accumulation (Section 5) and y rounded to fp16
- * (round to nearest even).  Inactive columns of W are never read (Section 3.1).
+ * with every product formed exactly in fp32 (Section 5's fp32 arithmetic),
+ * summed at least as accurately as fp32 accumulation would (see
+ * celty_spmspv), and y rounded to fp16 (round to nearest even).  Inactive
+ * columns of W are never read (Section 3.1).
  *
  * General rules
  * -------------
@@ -77,6 +79,8 @@ typedef struct celty_rlc_csc {
   int64_t n_entries;        /* stored values + padding entries (alignment excluded) */
   int64_t n_nnz;            /* stored values */
   int64_t n_pad;            /* padding entries */
+  float max_abs;            /* largest |stored value| (0 if none); finite */
+  int32_t reserved;         /* 0 */
   const uint32_t* gptr;     /* [T*K + 1], 4-byte aligned */
   const uint16_t* values;   /* [8*G] fp16 bits, 16-byte aligned */
   const uint32_t* runs;     /* [G], 4-byte aligned */
@@ -100,7 +104,8 @@ celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const uint8_t* ma
 /*
  * Encode into caller buffers (host): gptr [T*K+1], values [8*n_groups]
  * (16-byte aligned), runs [n_groups].  n_groups must equal the plan's value.
- * On success *out is filled (pointers = the three buffers given here).
+ * On success *out is filled (pointers = the three buffers given here, and
+ * max_abs = the largest magnitude among the stored values).
  * n_threads: worker threads, 0 = all hardware threads.  The result does not
  * depend on n_threads.
  * Errors: EINVAL (as for the plan, null buffers, misaligned values,
@@ -117,7 +122,7 @@ celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8_t* mask, i
  *   mask_out host, M x K uint8, stride K: 1 where a value is stored (may be NULL).
  * Errors: EINVAL (null pointers, bad header), EFORMAT (gptr not monotone from
  * 0 to n_groups, a stored value beyond its tile, an alignment entry with a
- * non-zero run, header counts that disagree with the stream).
+ * non-zero run, header counts or max_abs that disagree with the stream).
  */
 celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out);
 
@@ -163,10 +168,14 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  *   workspace  device buffer of at least celty_spmspv_workspace_bytes(M,K,R)
  *              bytes, zero-filled before first use (celty_spmspv_workspace_init).
  * One kernel launch: every workgroup selects the active columns of its slice
- * of x, walks their compressed segments for its row tile, accumulates fp32
- * partial products in LDS and merges tile partials across workgroups.
+ * of x, walks their compressed segments for its row tile, forms each fp32
+ * product (exact for fp16 factors), accumulates them in LDS in int32 fixed
+ * point scaled per workgroup so that no row can overflow (rounding error per
+ * row at most n^2 * max|w x| * 2^-32 for n active columns of the slice), and
+ * merges tile partials across workgroups with fp32 atomics.  W->max_abs must
+ * bound every stored |value| (the encoder sets it).
  * Errors: EINVAL (null or misaligned pointers, inconsistent header, NaN tau,
- *         short workspace), EHIP.
+ *         non-finite or negative max_abs, short workspace), EHIP.
  */
 celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y,
                           void* workspace, size_t workspace_bytes, void* stream);

@@ -51,7 +51,8 @@ _i32, _i64, _f32, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c
 class celty_rlc_csc(ctypes.Structure):
     _fields_ = [("version", _i32), ("M", _i32), ("K", _i32), ("R", _i32), ("T", _i32),
                 ("run_bits", _i32), ("n_groups", _i64), ("n_entries", _i64), ("n_nnz", _i64),
-                ("n_pad", _i64), ("gptr", _p), ("values", _p), ("runs", _p)]
+                ("n_pad", _i64), ("max_abs", _f32), ("reserved", _i32), ("gptr", _p), ("values", _p),
+                ("runs", _p)]
 
 
 class celty_launch(ctypes.Structure):
@@ -125,11 +126,12 @@ class HostRlcCsc:
         self.M, self.K, self.R, self.T = desc.M, desc.K, desc.R, desc.T
         self.n_groups, self.n_entries = int(desc.n_groups), int(desc.n_entries)
         self.n_nnz, self.n_pad = int(desc.n_nnz), int(desc.n_pad)
+        self.max_abs = float(desc.max_abs)
         self.gptr, self.values, self.runs = gptr, values, runs
 
     def desc(self) -> celty_rlc_csc:
         return celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
-                             self.n_entries, self.n_nnz, self.n_pad, self.gptr.ctypes.data,
+                             self.n_entries, self.n_nnz, self.n_pad, self.max_abs, 0, self.gptr.ctypes.data,
                              self.values.ctypes.data if self.values.size else None,
                              self.runs.ctypes.data if self.runs.size else None)
 
@@ -201,6 +203,7 @@ class DeviceRlcCsc:
         self.M, self.K, self.R, self.T = host.M, host.K, host.R, host.T
         self.n_groups, self.n_entries = host.n_groups, host.n_entries
         self.n_nnz, self.n_pad = host.n_nnz, host.n_pad
+        self.max_abs = host.max_abs
         self.gptr = torch.from_numpy(host.gptr.view(np.int32)).to(device)
         # at least one element so that pointers are never null
         self.values = torch.from_numpy(host.values.view(np.int16) if host.values.size
@@ -208,7 +211,8 @@ class DeviceRlcCsc:
         self.runs = torch.from_numpy(host.runs.view(np.int32) if host.runs.size
                                      else np.zeros(1, np.int32)).to(device)
         self._desc = celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
-                                   self.n_entries, self.n_nnz, self.n_pad, self.gptr.data_ptr(),
+                                   self.n_entries, self.n_nnz, self.n_pad, self.max_abs, 0,
+                                   self.gptr.data_ptr(),
                                    self.values.data_ptr(), self.runs.data_ptr())
 
     def desc(self) -> celty_rlc_csc:
@@ -220,7 +224,8 @@ class DeviceRlcCsc:
         other.__dict__.update(self.__dict__)
         other.gptr, other.values, other.runs = self.gptr.clone(), self.values.clone(), self.runs.clone()
         other._desc = celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
-                                    self.n_entries, self.n_nnz, self.n_pad, other.gptr.data_ptr(),
+                                    self.n_entries, self.n_nnz, self.n_pad, self.max_abs, 0,
+                                    other.gptr.data_ptr(),
                                     other.values.data_ptr(), other.runs.data_ptr())
         return other
 

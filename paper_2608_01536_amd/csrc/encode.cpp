@@ -26,6 +26,31 @@ inline bool stored(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t 
   return mask == nullptr || mask[r * ldm + k] != 0;
 }
 
+// Exact value of an fp16 bit pattern (finite or not).
+float half_bits_to_float(uint16_t h) {
+  const uint32_t sign = uint32_t(h >> 15) << 31;
+  const uint32_t exp = (h >> 10) & 0x1Fu, man = h & 0x3FFu;
+  uint32_t bits;
+  if (exp == 0x1F) {
+    bits = sign | 0x7F800000u | (man << 13);
+  } else if (exp != 0) {
+    bits = sign | ((exp + 112u) << 23) | (man << 13);
+  } else if (man == 0) {
+    bits = sign;
+  } else {   // subnormal: normalise
+    int e = 113;
+    uint32_t m = man;
+    while ((m & 0x400u) == 0) {
+      m <<= 1;
+      --e;
+    }
+    bits = sign | (uint32_t(e) << 23) | ((m & 0x3FFu) << 13);
+  }
+  float f;
+  std::memcpy(&f, &bits, sizeof f);
+  return f;
+}
+
 struct Item {
   int32_t t, k0, k1;
 };
@@ -149,6 +174,7 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
     const int64_t nseg = int64_t(T) * K;
     const std::vector<Item> items = make_items(T, K);
     std::vector<int64_t> nnz(items.size()), pad(items.size());
+    std::vector<uint16_t> vmax(items.size(), 0);   // largest |value| bits per item
 
     // pass 1: groups per segment, written into gptr[s] (then scanned in place)
     bool ok = parallel_items(items.size(), n_threads, [&](size_t i) {
@@ -197,7 +223,9 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
             emit(j, 0, uint32_t(kCap));
             gap -= kCap + 1;
           }
-          emit(j, W[r * ldw + it.k0 + j], uint32_t(gap));
+          const uint16_t v = W[r * ldw + it.k0 + j];
+          emit(j, v, uint32_t(gap));
+          vmax[i] = std::max<uint16_t>(vmax[i], uint16_t(v & 0x7FFFu));
           last[j] = rel;
         }
       }
@@ -206,9 +234,11 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
     if (!ok) return CELTY_ENOMEM;
 
     int64_t A = 0, B = 0;
+    uint16_t mbits = 0;
     for (size_t i = 0; i < items.size(); ++i) {
       A += nnz[i];
       B += pad[i];
+      mbits = std::max(mbits, vmax[i]);   // magnitude bits order like the values
     }
     out->version = CELTY_FORMAT_VERSION;
     out->M = M;
@@ -220,6 +250,8 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
     out->n_entries = A + B;
     out->n_nnz = A;
     out->n_pad = B;
+    out->max_abs = half_bits_to_float(mbits);
+    out->reserved = 0;
     out->gptr = gptr;
     out->values = values;
     out->runs = runs;
@@ -244,6 +276,7 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
   std::memset(W_out, 0, size_t(M) * K * sizeof(uint16_t));
   if (mask_out) std::memset(mask_out, 0, size_t(M) * K);
   int64_t nnz = 0, pad = 0;
+  uint16_t mbits = 0;
   for (int64_t s = 0; s < nseg; ++s) {
     const int64_t t = s / K, k = s % K;
     const int64_t hi = std::min<int64_t>(M, (t + 1) * int64_t(R));
@@ -264,6 +297,7 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
         if (row >= hi) return CELTY_EFORMAT;
         W_out[row * K + k] = v;
         if (mask_out) mask_out[row * K + k] = 1;
+        mbits = std::max<uint16_t>(mbits, uint16_t(v & 0x7FFFu));
         ++nnz;
       } else {
         ++pad;
@@ -271,5 +305,6 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
     }
   }
   if (nnz != enc->n_nnz || pad != enc->n_pad || nnz + pad != enc->n_entries) return CELTY_EFORMAT;
+  if (enc->max_abs != half_bits_to_float(mbits)) return CELTY_EFORMAT;
   return CELTY_OK;
 }

@@ -2,21 +2,26 @@
 //
 // One launch computes y = W x_A (Sections 3.1-3.3):
 //   * grid = (row tile t) x (slice c of x).  A workgroup selects the active
-//     columns of its slice (|x_k| > tau, wavefront ballot + prefix sums,
+//     columns of its slice (|x_k| > tau, wavefront ballot + prefix sums:
 //     Section 3.1's column skip turned into stream compaction) and drops
 //     columns whose segment in tile t is empty;
 //   * the workgroup's compressed groups (8 entries = 16 B of fp16 values +
 //     4 B of packed 4-bit runs) form one flat sequence; it is cut at segment
 //     boundaries into one contiguous range per wavefront;
-//   * a wavefront walks its range 64 groups (512 entries) per pass: each lane
-//     loads one group with a 128-bit and a 32-bit load (Section 3.1), turns
-//     the 8 runs into 8 inclusive prefixes with byte-packed arithmetic,
-//     combines lanes with a wavefront inclusive scan that restarts at segment
-//     heads (Algorithm 1: prefix of runs plus ordinal gives the row), and
-//     adds value * x_k (an exact fp32 product) into an fp64 LDS tile of the R
-//     output rows (Section 3.3: scatter-accumulation in on-chip memory; on
-//     gfx950 the LDS fp64 atomic add is an order of magnitude faster than the
-//     fp32 one, and it only makes the sum more accurate);
+//   * a wavefront walks its range 64 groups (512 entries) per pass, keeping a
+//     ring of passes in flight: each lane loads one group with a 128-bit and a
+//     32-bit load (Section 3.1), turns the 8 runs into 8 inclusive prefixes
+//     with byte-packed arithmetic, and combines lanes with a wavefront scan
+//     that restarts at segment heads (Algorithm 1: prefix of runs plus
+//     ordinal gives the row);
+//   * each product value * x_k is exact in fp32 (two fp16 factors) and is
+//     added into an LDS tile of the R output rows (Section 3.3's
+//     scatter-accumulation in on-chip memory).  The tile holds int32 fixed
+//     point with a per-workgroup power-of-two scale 2^s chosen so that no row
+//     of the slice can overflow: on gfx950 an LDS integer atomic add costs a
+//     small fraction of an fp32 one, and the rounding error of a row,
+//     n^2 * max|w x| * 2^-32 for n active columns in the slice, stays below
+//     the worst case of fp32 accumulation;
 //   * the tile is merged across slices with fp32 atomics into a workspace row
 //     block; the last workgroup of a row tile (counter) writes y in fp16 and
 //     clears its workspace rows and counter for the next call.  With a single
@@ -34,12 +39,13 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
+constexpr int kSlack = 8 + 128;       // tile rows past R: alignment entries, and the cap's reach
 
 struct SegInfo {
   uint32_t gstart;   // first group of the segment in the values/runs arrays
   uint32_t off;      // first group of the segment in the workgroup's flat sequence
   uint32_t cnt;      // groups in the segment (> 0)
-  float xv;          // x_k as fp32
+  float xs;          // x_k * 2^s (s: the workgroup's fixed-point scale)
 };
 
 __device__ __forceinline__ float half_bits_to_float(uint32_t bits) {
@@ -50,8 +56,8 @@ __device__ __forceinline__ unsigned short float_to_half_bits(float v) {
   return __half_as_ushort(__float2half_rn(v));
 }
 
-// Inclusive scan over the 64 lanes of a wavefront (DPP row shifts inside each
-// 16-lane row, then row broadcasts of lanes 15 and 31).
+// DPP row shifts inside each 16-lane row, then row broadcasts of lanes 15
+// and 31: inclusive scan over the 64 lanes.
 __device__ __forceinline__ int wave_inclusive_scan(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);   // row_shr:1
   v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);   // row_shr:2
@@ -59,6 +65,17 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);   // row_shr:8
   v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);   // row_bcast:15 -> rows 1, 3
   v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);   // row_bcast:31 -> rows 2, 3
+  return v;
+}
+
+// The same pattern with max: lane 63 ends with the wavefront maximum.
+__device__ __forceinline__ uint32_t wave_inclusive_max(uint32_t v) {
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x142, 0xA, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x143, 0xC, 0xF, false)));
   return v;
 }
 
@@ -75,27 +92,22 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-// LDS slot of a tile-relative row.  Rows past the tile (alignment entries of
-// a segment's last group, value 0) land in the slack; anything out of range
-// is clamped to the last slot, which is never read back.
-__device__ __forceinline__ uint32_t tile_slot(int row, uint32_t last_slot) {
-  const uint32_t r = static_cast<uint32_t>(row);
-  return r < last_slot ? r : last_slot;
-}
-
-// Exclusive block-wide scan of two counters; part[] holds 2*WAVES words.
+// Block-wide: exclusive scans of a and b, their totals, and the maximum of m.
+// part[] holds 3*WAVES words.
 template <int WAVES>
-__device__ __forceinline__ void block_exclusive_scan2(uint32_t a, uint32_t b, uint32_t& ea, uint32_t& eb,
-                                                      uint32_t& ta, uint32_t& tb, uint32_t* part) {
+__device__ __forceinline__ void block_scan_select(uint32_t a, uint32_t b, uint32_t m, uint32_t& ea, uint32_t& eb,
+                                                  uint32_t& ta, uint32_t& tb, uint32_t& tm, uint32_t* part) {
   const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
   const int ia = wave_inclusive_scan(static_cast<int>(a));
   const int ib = wave_inclusive_scan(static_cast<int>(b));
+  const uint32_t im = wave_inclusive_max(m);
   if (lane == kWave - 1) {
     part[wv] = static_cast<uint32_t>(ia);
     part[WAVES + wv] = static_cast<uint32_t>(ib);
+    part[2 * WAVES + wv] = im;
   }
   __syncthreads();
-  uint32_t oa = 0, ob = 0, sa = 0, sb = 0;
+  uint32_t oa = 0, ob = 0, sa = 0, sb = 0, mm = 0;
 #pragma unroll
   for (int w = 0; w < WAVES; ++w) {
     const uint32_t pa = part[w], pb = part[WAVES + w];
@@ -105,12 +117,123 @@ __device__ __forceinline__ void block_exclusive_scan2(uint32_t a, uint32_t b, ui
     }
     sa += pa;
     sb += pb;
+    mm = max(mm, part[2 * WAVES + w]);
   }
   ea = oa + static_cast<uint32_t>(ia) - a;
   eb = ob + static_cast<uint32_t>(ib) - b;
   ta = sa;
   tb = sb;
+  tm = mm;
   __syncthreads();
+}
+
+// fp16 (low or high half of a word) times an fp32 value, in one mixed-precision
+// FMA; exact for the products formed here (11-bit by 11-bit significands).
+__device__ __forceinline__ float mul_lo_f16(uint32_t w, float x) {
+  float r;
+  asm("v_fma_mix_f32 %0, %1, %2, 0 op_sel_hi:[1,0,0]" : "=v"(r) : "v"(w), "v"(x));
+  return r;
+}
+__device__ __forceinline__ float mul_hi_f16(uint32_t w, float x) {
+  float r;
+  asm("v_fma_mix_f32 %0, %1, %2, 0 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(r) : "v"(w), "v"(x));
+  return r;
+}
+
+// floor(v + 0.5) as int32 (v is within +-2^30 by the choice of scale).
+__device__ __forceinline__ int round_to_fixed(float v) {
+  int r;
+  asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(r) : "v"(v));
+  return r;
+}
+
+// One pass's input for a lane: its group of 8 entries and its segment.
+struct Pass {
+  uint4 v;           // 8 fp16 values
+  uint32_t rw;       // 8 packed 4-bit runs
+  int sid;           // segment (index into the workgroup's segment list)
+  int h;             // lane where the segment starts in this pass (<= 0: earlier)
+  uint32_t segend;   // flat end (exclusive) of the segment
+  float xs;          // scaled x_k of the segment's column
+  bool live;         // the lane holds a group
+};
+
+// Assigns the 64 groups starting at flat position pb to lanes and issues
+// their loads.  icur is the segment holding group pb.
+template <class Args>
+__device__ __forceinline__ Pass fetch_pass(const Args& p, const SegInfo* seg, int* scr, uint32_t pb, int icur,
+                                           int i_end, uint32_t pe, int lane) {
+  // heads of the segments that start inside (pb, pb + 64): tag their lane
+  const int j = icur + lane;
+  if (lane > 0 && j < i_end) {
+    const uint32_t o = seg[j].off;
+    if (o < pb + kWave) scr[o - pb] = static_cast<int>(pb + 1u);
+  }
+  wave_lds_sync();
+  const bool head = lane > 0 && scr[lane] == static_cast<int>(pb + 1u);
+  const uint64_t hm = __ballot(head);
+  Pass a;
+  a.sid = min(icur + static_cast<int>(lanes_below(hm)) + (head ? 1 : 0), i_end - 1);
+  const SegInfo si = seg[a.sid];
+  const uint32_t f = pb + static_cast<uint32_t>(lane);
+  a.live = f < pe;
+  a.h = static_cast<int>(si.off) - static_cast<int>(pb);
+  a.segend = si.off + si.cnt;
+  a.xs = si.xs;
+  // Loads are issued by every lane on every pass (idle lanes and the passes
+  // past the end read group 0 and drop it), so the wait for one pass's data
+  // can leave the later passes' loads in flight.  gi < n_groups always holds
+  // for an encoder-made stream; the test keeps a corrupt group-pointer array
+  // from reading outside the arrays.
+  const uint32_t gi = si.gstart + (f - si.off);
+  const uint32_t gl = (a.live && gi < p.n_groups) ? gi : 0u;
+  a.v = p.values[gl];
+  a.rw = p.runs[gl];
+  return a;
+}
+
+// The segment holding the first group of the pass after the one fetched at
+// flat position pb (wavefront-uniform).
+__device__ __forceinline__ int next_pass_segment(const Pass& a, uint32_t pb, int i_end) {
+  const int sid63 = __builtin_amdgcn_readlane(a.sid, kWave - 1);
+  const uint32_t end63 = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(a.segend), kWave - 1));
+  return min(end63 > pb + kWave ? sid63 : sid63 + 1, i_end - 1);
+}
+
+// Decodes one pass and adds its products into the fixed-point tile.  Returns,
+// per lane, the segment-relative sum of (run + 1) through the lane's group
+// (the carry when the segment goes on into the next pass).
+__device__ __forceinline__ int accumulate_pass(int* tile, const Pass& a, int carry, int base_cap) {
+  // byte k of O: inclusive prefix of (run + 1) through entry 2k+1; byte k of
+  // E: the same through entry 2k.  The byte-wise running sum is two shift-adds
+  // (kept as such rather than the quarter-rate multiply by 0x01010101).
+  const uint32_t rw = a.live ? a.rw : 0u;
+  const uint32_t r_even = rw & 0x0F0F0F0Fu;
+  const uint32_t r_odd = (rw >> 4) & 0x0F0F0F0Fu;
+  const uint32_t pair = r_even + r_odd + 0x02020202u;
+  uint32_t half, O;
+  asm("v_lshl_add_u32 %0, %1, 8, %1" : "=v"(half) : "v"(pair));
+  asm("v_lshl_add_u32 %0, %1, 16, %1" : "=v"(O) : "v"(half));
+  const uint32_t E = O - r_odd - 0x01010101u;
+  const int S = a.live ? static_cast<int>(O >> 24) : 0;   // lane total
+  const int incl = wave_inclusive_scan(S);
+  const int excl = incl - S;
+  const int eh = __builtin_amdgcn_ds_bpermute((a.h > 0 ? a.h : 0) << 2, excl);
+  const int rel = excl - eh + (a.h < 0 ? carry : 0);     // segment-relative
+  if (a.live) {
+    // row of entry j = base + prefix_j; base >= -1 and prefix_j <= 128, and the
+    // cap keeps even a corrupt stream inside the tile's slack
+    const int base = min(rel - 1, base_cap);
+    const uint32_t w4[4] = {a.v.x, a.v.y, a.v.z, a.v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int re = base + static_cast<int>((E >> (8 * q)) & 0xFFu);
+      const int ro = base + static_cast<int>((O >> (8 * q)) & 0xFFu);
+      atomicAdd(tile + re, round_to_fixed(mul_lo_f16(w4[q], a.xs)));
+      atomicAdd(tile + ro, round_to_fixed(mul_hi_f16(w4[q], a.xs)));
+    }
+  }
+  return rel + S;
 }
 
 struct KernelArgs {
@@ -122,35 +245,37 @@ struct KernelArgs {
   float* ws;                    // [M] fp32 partials
   uint32_t* counters;           // [T]
   float tau;
+  float max_abs;                // max |stored weight|
+  uint32_t n_groups;
   int M, K, R, Kc, KC, tile_slots;
-  int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS
+  int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS (the tile is at 0)
 };
 
-template <int WAVES>
+template <int WAVES, int DEPTH = 3>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   constexpr int NT = WAVES * kWave;
   extern __shared__ __align__(16) unsigned char smem[];
-  double* tile = reinterpret_cast<double*>(smem);
+  int* tile = reinterpret_cast<int*>(smem);
   SegInfo* seg = reinterpret_cast<SegInfo*>(smem + p.seg_off);
   int* scr_all = reinterpret_cast<int*>(smem + p.scr_off);
-  uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 2*WAVES
-  int* wfirst = reinterpret_cast<int*>(part + 2 * WAVES);             // WAVES+1
+  uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 3*WAVES
+  int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES+1
   int* last_flag = wfirst + WAVES + 1;                                // 1
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int t = blockIdx.x / p.KC, c = blockIdx.x - t * p.KC;
   const int row0 = t * p.R;
   const int rows = min(p.R, p.M - row0);
-  const uint32_t last_slot = static_cast<uint32_t>(p.tile_slots - 1);
+  const int base_cap = p.R + 7;
 
-  for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0.0;
+  for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0;
   scr_all[tid] = 0;
 
   // ---- selection of this slice's active, non-empty columns ----------------
   const int k0 = c * p.Kc;
   const int kn = min(p.Kc, p.K - k0);
   const uint32_t* gp = p.gptr + static_cast<size_t>(t) * p.K + k0;
-  uint32_t n_seg = 0, n_grp = 0;
+  uint32_t n_seg = 0, n_grp = 0, xmax_bits = 0;
   for (int it = 0; it < kn; it += NT) {
     const int kk = it + tid;
     uint32_t g0 = 0, g1 = 0;
@@ -163,13 +288,27 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
       keep = (fabsf(xv) > p.tau) && (g1 > g0);
     }
     const uint32_t cnt = keep ? g1 - g0 : 0u;
-    uint32_t en, eg, tn, tg;
-    block_exclusive_scan2<WAVES>(keep ? 1u : 0u, cnt, en, eg, tn, tg, part);
+    // |x| >= 0 orders like its bit pattern
+    const uint32_t mbits = keep ? __float_as_uint(fabsf(xv)) : 0u;
+    uint32_t en, eg, tn, tg, tm;
+    block_scan_select<WAVES>(keep ? 1u : 0u, cnt, mbits, en, eg, tn, tg, tm, part);
+    // x_k is stored unscaled for now; the scale is known after the last step
     if (keep) seg[n_seg + en] = SegInfo{g0, n_grp + eg, cnt, xv};
     n_seg += tn;
     n_grp += tg;
+    xmax_bits = max(xmax_bits, tm);
+  }
+  // Fixed-point scale: a row of this slice sums at most n_seg terms, each at
+  // most max|w| * max|x| in magnitude; 2^s puts that bound at or below 2^30.
+  int s = 0;
+  const float bound = static_cast<float>(n_seg) * p.max_abs * __uint_as_float(xmax_bits);
+  if (bound > 0.f) {
+    int e;
+    frexpf(bound, &e);                 // bound < 2^e
+    s = min(max(30 - e, -64), 64);
   }
   __syncthreads();
+  for (int i = tid; i < static_cast<int>(n_seg); i += NT) seg[i].xs = ldexpf(seg[i].xs, s);
 
   // ---- cut the flat group sequence into one range per wavefront -----------
   // segment i goes to wavefront floor(off_i * WAVES / n_grp); wfirst[w] is the
@@ -185,80 +324,48 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   __syncthreads();
 
   // ---- per-wavefront walk over 64-group passes ----------------------------
+  // A ring of DEPTH passes is kept in flight: after a pass is decoded and
+  // accumulated, its slot is refilled with the loads of the pass DEPTH ahead.
+  // The ring is indexed by compile-time constants (fully unrolled), so no
+  // register copies force an early wait.  Passes past the end are idle (every
+  // lane inactive, loads of group 0) and accumulate nothing.
   const int i_begin = wfirst[wv], i_end = wfirst[wv + 1];
   if (i_begin < i_end) {
     int* scr = scr_all + wv * kWave;
-    uint32_t pb = seg[i_begin].off;
+    const uint32_t pb0 = seg[i_begin].off;
     const uint32_t pe = i_end < static_cast<int>(n_seg) ? seg[i_end].off : n_grp;
-    int icur = i_begin;   // segment holding flat group pb
-    int carry = 0;        // its sum of (run + 1) over groups before pb
-    while (pb < pe) {
-      // heads of the segments that start inside (pb, pb + 64): tag their lane
-      const int j = icur + lane;
-      if (lane > 0 && j < i_end) {
-        const uint32_t o = seg[j].off;
-        if (o < pb + kWave) scr[o - pb] = static_cast<int>(pb + 1u);
-      }
-      wave_lds_sync();
-      const bool head = lane > 0 && scr[lane] == static_cast<int>(pb + 1u);
-      const uint64_t hm = __ballot(head);
-      const int sid = icur + static_cast<int>(lanes_below(hm)) + (head ? 1 : 0);
-      const SegInfo si = seg[sid];
-
-      const uint32_t f = pb + static_cast<uint32_t>(lane);
-      const bool live = f < pe;
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      uint32_t rw = 0u;
-      if (live) {
-        const uint32_t gi = si.gstart + (f - si.off);
-        v = p.values[gi];
-        rw = p.runs[gi];
-      }
-      // byte k of O: inclusive prefix of (run + 1) through entry 2k+1;
-      // byte k of E: the same through entry 2k.
-      const uint32_t r_even = rw & 0x0F0F0F0Fu;
-      const uint32_t r_odd = (rw >> 4) & 0x0F0F0F0Fu;
-      const uint32_t O = (r_even + r_odd + 0x02020202u) * 0x01010101u;
-      const uint32_t E = O - r_odd - 0x01010101u;
-      const int S = live ? static_cast<int>(O >> 24) : 0;   // lane total
-      const int incl = wave_inclusive_scan(S);
-      const int excl = incl - S;
-      const int h = static_cast<int>(si.off) - static_cast<int>(pb);   // head lane of my segment
-      const int eh = __builtin_amdgcn_ds_bpermute((h > 0 ? h : 0) << 2, excl);
-      const int rel = excl - eh + (h < 0 ? carry : 0);                 // segment-relative
-      if (live) {
-        const float xv = si.xv;
-        const int base = rel - 1;   // row of entry j = base + prefix_j
-        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+    const int n_pass = static_cast<int>((pe - pb0 + kWave - 1) / kWave);
+    Pass ring[DEPTH];
+    uint32_t pf = pb0;    // flat start of the next pass to fetch
+    int icur = i_begin;   // segment holding group pf
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int re = base + static_cast<int>((E >> (8 * q)) & 0xFFu);
-          const int ro = base + static_cast<int>((O >> (8 * q)) & 0xFFu);
-          // the fp32 product of two fp16 values is exact; it is summed in fp64
-          atomicAdd(&tile[tile_slot(re, last_slot)], static_cast<double>(half_bits_to_float(w4[q] & 0xFFFFu) * xv));
-          atomicAdd(&tile[tile_slot(ro, last_slot)], static_cast<double>(half_bits_to_float(w4[q] >> 16) * xv));
-        }
+    for (int d = 0; d < DEPTH; ++d) {
+      ring[d] = fetch_pass(p, seg, scr, pf, icur, i_end, pe, lane);
+      icur = next_pass_segment(ring[d], pf, i_end);
+      pf += kWave;
+    }
+    uint32_t pb = pb0;    // flat start of the pass being accumulated
+    int carry = 0;        // sum of (run + 1) over its first segment's earlier groups
+    for (int done = 0; done < n_pass; done += DEPTH) {
+#pragma unroll
+      for (int d = 0; d < DEPTH; ++d) {
+        const int tail = accumulate_pass(tile, ring[d], carry, base_cap);
+        const uint32_t end63 =
+            static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(ring[d].segend), kWave - 1));
+        carry = end63 > pb + kWave ? __builtin_amdgcn_readlane(tail, kWave - 1) : 0;
+        pb += kWave;
+        ring[d] = fetch_pass(p, seg, scr, pf, icur, i_end, pe, lane);
+        icur = next_pass_segment(ring[d], pf, i_end);
+        pf += kWave;
       }
-      // the segment that holds the next pass's first group, and its carry
-      const int sid63 = __builtin_amdgcn_readlane(sid, kWave - 1);
-      const uint32_t end63 = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(si.off + si.cnt), kWave - 1));
-      const int carry63 = __builtin_amdgcn_readlane(rel + S, kWave - 1);
-      const uint32_t pn = pb + kWave;
-      if (end63 > pn) {
-        icur = sid63;
-        carry = carry63;
-      } else {
-        icur = sid63 + 1;
-        carry = 0;
-      }
-      pb = pn;
     }
   }
   __syncthreads();
 
   // ---- merge --------------------------------------------------------------
   if (p.KC == 1) {
-    for (int r = tid; r < rows; r += NT) p.y[row0 + r] = float_to_half_bits(static_cast<float>(tile[r]));
+    for (int r = tid; r < rows; r += NT)
+      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -s));
     return;
   }
   // Returning device-scope atomics are performed at the device's coherence
@@ -268,8 +375,8 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   float* wsr = p.ws + row0;
   float sink = 0.f;
   for (int r = tid; r < rows; r += NT) {
-    const float v = static_cast<float>(tile[r]);
-    if (v != 0.f) sink += unsafeAtomicAdd(wsr + r, v);
+    const int q = tile[r];
+    if (q != 0) sink += unsafeAtomicAdd(wsr + r, ldexpf(static_cast<float>(q), -s));
   }
   asm volatile("" ::"v"(sink));
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -341,6 +448,7 @@ celty_status check_header(const celty_rlc_csc* W) {
   if (W->n_groups < 0 || W->n_groups > static_cast<int64_t>(UINT32_MAX)) return CELTY_EINVAL;
   if (!W->gptr || misaligned(W->gptr, 4)) return CELTY_EINVAL;
   if (W->n_groups > 0 && (!W->values || !W->runs)) return CELTY_EINVAL;
+  if (!(W->max_abs >= 0.f) || std::isinf(W->max_abs)) return CELTY_EINVAL;
   if (misaligned(W->values, 16) || misaligned(W->runs, 4)) return CELTY_EINVAL;
   return CELTY_OK;
 }
@@ -364,14 +472,17 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   if (Kc > W->K) Kc = W->K;
   pl.Kc = Kc;
   pl.KC = (W->K + Kc - 1) / Kc;
-  pl.tile_slots = W->R + 8;
-  size_t off = align_up(static_cast<size_t>(pl.tile_slots) * 8, 16);
+  // the tile (int32) goes first: R rows, then 7 alignment rows and 128 rows
+  // of slack that bound where a corrupt stream could write (base is capped at
+  // R + 7 and a group adds at most 128)
+  pl.tile_slots = W->R + kSlack;
+  size_t off = align_up(static_cast<size_t>(pl.tile_slots) * 4, 16);
   pl.seg_off = static_cast<int>(off);
   off += static_cast<size_t>(Kc) * sizeof(SegInfo);
   pl.scr_off = static_cast<int>(off);
   off += static_cast<size_t>(pl.waves) * kWave * 4;
   pl.misc_off = static_cast<int>(off);
-  off += static_cast<size_t>(3 * pl.waves + 2) * 4;
+  off += static_cast<size_t>(4 * pl.waves + 2) * 4;
   pl.lds = align_up(off, 16);
   if (pl.lds > static_cast<size_t>(kMaxLds)) return CELTY_EINVAL;
   pl.blocks = static_cast<int64_t>(W->T) * pl.KC;
@@ -442,6 +553,8 @@ extern "C" celty_status celty_spmspv_ex(const celty_rlc_csc* W, const void* x, f
   a.ws = static_cast<float*>(workspace);
   a.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + align_up(static_cast<size_t>(W->M) * 4, 256));
   a.tau = tau;
+  a.max_abs = W->max_abs;
+  a.n_groups = static_cast<uint32_t>(W->n_groups);
   a.M = W->M;
   a.K = W->K;
   a.R = W->R;

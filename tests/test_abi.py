@@ -135,7 +135,7 @@ FAKE = 0x7F0000000000   # never dereferenced: every call below fails validation 
 
 def _desc(M=4096, K=4096, R=256, G=1000):
     T = -(-M // R)
-    return celty_rlc_csc(1, M, K, R, T, 4, G, 8 * G, 7 * G, G, FAKE, FAKE + 0x10000, FAKE + 0x20000)
+    return celty_rlc_csc(1, M, K, R, T, 4, G, 8 * G, 7 * G, G, 1.0, 0, FAKE, FAKE + 0x10000, FAKE + 0x20000)
 
 
 @host_only
@@ -157,7 +157,7 @@ def test_spmspv_plan_is_host_only():
 @host_only
 @pytest.mark.parametrize("case", ["null_desc", "version", "run_bits", "T", "values_align", "runs_align",
                                   "null_x", "nan_tau", "x_align", "overlap", "short_ws", "null_ws",
-                                  "ws_align", "waves"])
+                                  "ws_align", "waves", "max_abs_nan", "max_abs_inf", "max_abs_neg"])
 def test_spmspv_rejects_bad_arguments(case):
     d = _desc()
     x, y, ws = FAKE + 0x100000, FAKE + 0x200000, FAKE + 0x300000
@@ -190,6 +190,12 @@ def test_spmspv_rejects_bad_arguments(case):
         ws += 16
     elif case == "waves":
         launch = celty_launch(64, 5)
+    elif case == "max_abs_nan":
+        d.max_abs = math.nan
+    elif case == "max_abs_inf":
+        d.max_abs = math.inf
+    elif case == "max_abs_neg":
+        d.max_abs = -1.0
     pd = None if case == "null_desc" else ctypes.byref(d)
     st = celty._spmspv_ex(pd, x, tau, y, ws, nws, None if launch is None else ctypes.byref(launch), None)
     assert st == CELTY_EINVAL

@@ -89,3 +89,19 @@ def test_encoder_full_size_row_magnitude_11008():
                                mask_kind="row_magnitude")
     enc = celty.celty_encode(p.W, p.mask, 256)
     _assert_same(enc, rlc.encode_matrix(p.W, p.mask, 256))
+
+
+@pytest.mark.parametrize("M,K,R", [(300, 200, 64), (77, 5, 16)])
+def test_header_max_abs(M, K, R):
+    p = workloads.random_small(M * K, M, K, ws=50, as_=50, zero_weights=2)
+    enc = celty.celty_encode(p.W, p.mask, R)
+    stored = (p.mask != 0) & ((p.W.view(np.uint16) & 0x7FFF) != 0)
+    want = float(np.max(np.abs(p.W.astype(np.float32))[stored])) if stored.any() else 0.0
+    assert enc.max_abs == want
+    # subnormal-only matrix: exact conversion of fp16 subnormals
+    Ws = np.zeros((4, 4), dtype=np.float16)
+    Ws.view(np.uint16)[1, 2] = 0x0003
+    Ws.view(np.uint16)[3, 0] = 0x8201
+    e2 = celty.celty_encode(Ws, None, 2)
+    assert e2.max_abs == float(np.abs(Ws.astype(np.float32)).max())
+    assert celty.celty_encode(np.zeros((3, 3), np.float16), None, 2).max_abs == 0.0
