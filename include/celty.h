@@ -139,14 +139,16 @@ celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* ma
 celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int32_t* count,
                           void* stream);
 
-/* Launch shape of celty_spmspv_ex.  Zero fields mean "choose automatically". */
+/* Launch shape of celty_spmspv_ex.  Zero fields mean "choose automatically".
+ * The K columns are cut into ceil(K / cols_per_block) slices, at most 63
+ * (the merge counts slices in one byte of a 64-bit word). */
 typedef struct celty_launch {
   int32_t cols_per_block;   /* columns of x one workgroup scans (1..4096) */
   int32_t waves_per_block;  /* 2, 4, 8 or 16 wavefronts of 64 lanes */
 } celty_launch;
 
-/* Bytes of device workspace celty_spmspv needs for this shape (M floats of
- * partial sums plus T counters, each rounded to 256 bytes). */
+/* Bytes of device workspace celty_spmspv needs for this shape: one 64-bit
+ * merge slot per output row, rounded up to 256 bytes. */
 size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R);
 
 /*
@@ -172,10 +174,13 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  * product (exact for fp16 factors), accumulates them in LDS in int32 fixed
  * point scaled per workgroup so that no row can overflow (rounding error per
  * row at most n^2 * max|w x| * 2^-32 for n active columns of the slice), and
- * merges tile partials across workgroups with fp32 atomics.  W->max_abs must
- * bound every stored |value| (the encoder sets it).
+ * merges the slices of a row tile with one returning 64-bit atomic per row
+ * (fixed point at a launch-wide scale, with an arrival count): the slice
+ * that arrives last at a row writes y[row] and clears the slot.  W->max_abs
+ * must bound every stored |value| (the encoder sets it).
  * Errors: EINVAL (null or misaligned pointers, inconsistent header, NaN tau,
- *         non-finite or negative max_abs, short workspace), EHIP.
+ *         non-finite or negative max_abs, short workspace, more than 63
+ *         column slices), EHIP.
  */
 celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y,
                           void* workspace, size_t workspace_bytes, void* stream);

@@ -289,9 +289,14 @@ def celty_spmspv_plan(W, launch=None) -> dict:
 def default_tile_rows(M: int, K: int) -> int:
     """Tile height R used for the benchmark encodings (rows per LDS tile).
 
-    256 rows keep segments short enough for row-tile parallelism on 256 CUs
-    while the 8-entry alignment costs only a few percent of the bytes."""
-    return 256
+    Small matrices need short tiles for enough row-tile parallelism on 256
+    CUs; tall ones take longer tiles, which spend fewer bytes on group
+    pointers and on the 8-entry alignment of each segment."""
+    if M <= 4096:
+        return 128
+    if M <= 16384:
+        return 256
+    return 512
 
 
 __all__ = [

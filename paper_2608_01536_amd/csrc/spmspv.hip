@@ -40,6 +40,7 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kSlack = 8 + 128;       // tile rows past R: alignment entries, and the cap's reach
+constexpr int kMaxSlices = 63;        // column slices per row tile (merge ticket count byte)
 
 struct SegInfo {
   uint32_t gstart;   // first group of the segment in the values/runs arrays
@@ -159,34 +160,43 @@ struct Pass {
 };
 
 // Assigns the 64 groups starting at flat position pb to lanes and issues
-// their loads.  icur is the segment holding group pb.
+// their loads.  icur is the segment holding group pb.  A pass at or past the
+// end (pb >= pe) skips the assignment and has every lane idle.
 template <class Args>
 __device__ __forceinline__ Pass fetch_pass(const Args& p, const SegInfo* seg, int* scr, uint32_t pb, int icur,
                                            int i_end, uint32_t pe, int lane) {
-  // heads of the segments that start inside (pb, pb + 64): tag their lane
-  const int j = icur + lane;
-  if (lane > 0 && j < i_end) {
-    const uint32_t o = seg[j].off;
-    if (o < pb + kWave) scr[o - pb] = static_cast<int>(pb + 1u);
-  }
-  wave_lds_sync();
-  const bool head = lane > 0 && scr[lane] == static_cast<int>(pb + 1u);
-  const uint64_t hm = __ballot(head);
   Pass a;
-  a.sid = min(icur + static_cast<int>(lanes_below(hm)) + (head ? 1 : 0), i_end - 1);
-  const SegInfo si = seg[a.sid];
-  const uint32_t f = pb + static_cast<uint32_t>(lane);
-  a.live = f < pe;
-  a.h = static_cast<int>(si.off) - static_cast<int>(pb);
-  a.segend = si.off + si.cnt;
-  a.xs = si.xs;
-  // Loads are issued by every lane on every pass (idle lanes and the passes
-  // past the end read group 0 and drop it), so the wait for one pass's data
-  // can leave the later passes' loads in flight.  gi < n_groups always holds
-  // for an encoder-made stream; the test keeps a corrupt group-pointer array
-  // from reading outside the arrays.
-  const uint32_t gi = si.gstart + (f - si.off);
-  const uint32_t gl = (a.live && gi < p.n_groups) ? gi : 0u;
+  a.sid = icur;
+  a.h = 0;
+  a.segend = pe;
+  a.xs = 0.f;
+  a.live = false;
+  uint32_t gl = 0u;
+  if (pb < pe) {   // wavefront-uniform
+    // heads of the segments that start inside (pb, pb + 64): tag their lane
+    const int j = icur + lane;
+    if (lane > 0 && j < i_end) {
+      const uint32_t o = seg[j].off;
+      if (o < pb + kWave) scr[o - pb] = static_cast<int>(pb + 1u);
+    }
+    wave_lds_sync();
+    const bool head = lane > 0 && scr[lane] == static_cast<int>(pb + 1u);
+    const uint64_t hm = __ballot(head);
+    a.sid = min(icur + static_cast<int>(lanes_below(hm)) + (head ? 1 : 0), i_end - 1);
+    const SegInfo si = seg[a.sid];
+    const uint32_t f = pb + static_cast<uint32_t>(lane);
+    a.live = f < pe;
+    a.h = static_cast<int>(si.off) - static_cast<int>(pb);
+    a.segend = si.off + si.cnt;
+    a.xs = si.xs;
+    // gi < n_groups always holds for an encoder-made stream; the test keeps a
+    // corrupt group-pointer array from reading outside the arrays
+    const uint32_t gi = si.gstart + (f - si.off);
+    gl = (a.live && gi < p.n_groups) ? gi : 0u;
+  }
+  // Loads are issued by every lane of every pass (idle lanes and idle passes
+  // read group 0 and drop it), so the wait for one pass's data can leave the
+  // later passes' loads in flight.
   a.v = p.values[gl];
   a.rw = p.runs[gl];
   return a;
@@ -203,7 +213,8 @@ __device__ __forceinline__ int next_pass_segment(const Pass& a, uint32_t pb, int
 // Decodes one pass and adds its products into the fixed-point tile.  Returns,
 // per lane, the segment-relative sum of (run + 1) through the lane's group
 // (the carry when the segment goes on into the next pass).
-__device__ __forceinline__ int accumulate_pass(int* tile, const Pass& a, int carry, int base_cap) {
+__device__ __forceinline__ int accumulate_pass(int* tile, const Pass& a, int carry, int base_cap, bool idle) {
+  if (idle) return 0;   // wavefront-uniform
   // byte k of O: inclusive prefix of (run + 1) through entry 2k+1; byte k of
   // E: the same through entry 2k.  The byte-wise running sum is two shift-adds
   // (kept as such rather than the quarter-rate multiply by 0x01010101).
@@ -242,10 +253,10 @@ struct KernelArgs {
   const uint32_t* runs;
   const unsigned short* x;      // fp16 bits
   unsigned short* y;            // fp16 bits
-  float* ws;                    // [M] fp32 partials
-  uint32_t* counters;           // [T]
+  unsigned long long* ws;       // [M] merge tickets (see the merge below)
   float tau;
   float max_abs;                // max |stored weight|
+  int s_glob;                   // fixed-point scale of the cross-slice merge
   uint32_t n_groups;
   int M, K, R, Kc, KC, tile_slots;
   int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS (the tile is at 0)
@@ -260,7 +271,6 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   int* scr_all = reinterpret_cast<int*>(smem + p.scr_off);
   uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 3*WAVES
   int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES+1
-  int* last_flag = wfirst + WAVES + 1;                                // 1
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int t = blockIdx.x / p.KC, c = blockIdx.x - t * p.KC;
@@ -311,11 +321,14 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   for (int i = tid; i < static_cast<int>(n_seg); i += NT) seg[i].xs = ldexpf(seg[i].xs, s);
 
   // ---- cut the flat group sequence into one range per wavefront -----------
-  // segment i goes to wavefront floor(off_i * WAVES / n_grp); wfirst[w] is the
+  // segment i goes to wavefront ~floor(off_i * WAVES / n_grp); wfirst[w] is the
   // first segment of wavefront w, wfirst[WAVES] = n_seg.
+  // (any non-decreasing map of offsets to [0, WAVES) is valid; rounding in the
+  // float product keeps it non-decreasing)
+  const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
   for (int i = tid; i < static_cast<int>(n_seg); i += NT) {
-    const int wi = static_cast<int>((static_cast<uint64_t>(seg[i].off) * WAVES) / n_grp);
-    const int wp = i == 0 ? -1 : static_cast<int>((static_cast<uint64_t>(seg[i - 1].off) * WAVES) / n_grp);
+    const int wi = min(static_cast<int>(static_cast<float>(seg[i].off) * wscale), WAVES - 1);
+    const int wp = i == 0 ? -1 : min(static_cast<int>(static_cast<float>(seg[i - 1].off) * wscale), WAVES - 1);
     for (int w = wp + 1; w <= wi; ++w) wfirst[w] = i;
     if (i == static_cast<int>(n_seg) - 1)
       for (int w = wi + 1; w <= WAVES; ++w) wfirst[w] = static_cast<int>(n_seg);
@@ -349,7 +362,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
     for (int done = 0; done < n_pass; done += DEPTH) {
 #pragma unroll
       for (int d = 0; d < DEPTH; ++d) {
-        const int tail = accumulate_pass(tile, ring[d], carry, base_cap);
+        const int tail = accumulate_pass(tile, ring[d], carry, base_cap, pb >= pe);
         const uint32_t end63 =
             static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(ring[d].segend), kWave - 1));
         carry = end63 > pb + kWave ? __builtin_amdgcn_readlane(tail, kWave - 1) : 0;
@@ -368,31 +381,33 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
       p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -s));
     return;
   }
-  // Returning device-scope atomics are performed at the device's coherence
-  // point before they return; waiting for them (workgroup-scope release) and
-  // then bumping the tile counter orders them before the last workgroup's
-  // device-coherent loads, without writing back or invalidating the L2s.
-  float* wsr = p.ws + row0;
-  float sink = 0.f;
+  // Every slice adds one ticket per row with a returning 64-bit atomic: its
+  // partial sum as fixed point at the launch-wide scale 2^s_glob (|v| <= 2^48
+  // by the choice of s_glob) plus a bias of 2^49 that keeps each ticket
+  // positive, and 1 in the count byte (bits 56..63).  The slice whose atomic
+  // returns count KC-1 is the last for that row: old + its ticket is the
+  // complete sum, so it writes y and clears the slot for the next call.
+  // KC <= 63 keeps the biased sum below 2^56.
+  constexpr long long kBias = 1ll << 49;
+  constexpr unsigned long long kCount = 1ull << 56;
+  const int shift = p.s_glob - s;
   for (int r = tid; r < rows; r += NT) {
-    const int q = tile[r];
-    if (q != 0) sink += unsafeAtomicAdd(wsr + r, ldexpf(static_cast<float>(q), -s));
-  }
-  asm volatile("" ::"v"(sink));
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t old = atomicAdd(p.counters + t, 1u);
-    *last_flag = old == static_cast<uint32_t>(p.KC - 1);
-  }
-  __syncthreads();
-  if (*last_flag) {
-    for (int r = tid; r < rows; r += NT) {
-      const float v = __hip_atomic_load(wsr + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      p.y[row0 + r] = float_to_half_bits(v);
-      __hip_atomic_store(wsr + r, 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const long long q = tile[r];
+    long long v;
+    if (shift >= 0) {
+      v = q * (1ll << shift);
+    } else {   // round half up onto the coarser grid
+      const int rs = -shift;
+      v = rs > 62 ? 0 : ((q + (1ll << (rs - 1))) >> rs);
     }
-    if (tid == 0) __hip_atomic_store(p.counters + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long ticket = kCount + static_cast<unsigned long long>(v + kBias);
+    const unsigned long long old = atomicAdd(p.ws + row0 + r, ticket);
+    if ((old >> 56) == static_cast<unsigned long long>(p.KC - 1)) {
+      const long long total = static_cast<long long>((old & (kCount - 1)) + (ticket & (kCount - 1))) -
+                              static_cast<long long>(p.KC) * kBias;
+      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(total), -p.s_glob));
+      p.ws[row0 + r] = 0ull;
+    }
   }
 }
 
@@ -456,22 +471,21 @@ celty_status check_header(const celty_rlc_csc* W) {
 celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl) {
   if (celty_status st = check_header(W)) return st;
   pl.T = W->T;
-  pl.waves = (cfg && cfg->waves_per_block) ? cfg->waves_per_block : 4;
+  pl.waves = (cfg && cfg->waves_per_block) ? cfg->waves_per_block : 8;
   if (pl.waves != 2 && pl.waves != 4 && pl.waves != 8 && pl.waves != 16) return CELTY_EINVAL;
   int Kc = cfg ? cfg->cols_per_block : 0;
   if (Kc == 0) {
-    // aim at ~2048 workgroups (8 per CU) with slices of 64..1024 columns
-    const int64_t want = (2048 + W->T - 1) / W->T;
-    int64_t kc = (W->K + want - 1) / want;
-    kc = (kc + 63) / 64 * 64;
-    if (kc < 64) kc = 64;
-    if (kc > 1024) kc = 1024;
+    // slices of 512 columns (fewer than 64 slices: the merge's count byte)
+    int64_t kc = 512;
+    const int64_t min_kc = (W->K + kMaxSlices - 1) / kMaxSlices;
+    if (kc < min_kc) kc = (min_kc + 63) / 64 * 64;
     Kc = static_cast<int>(kc);
   }
   if (Kc < 1 || Kc > 4096) return CELTY_EINVAL;
   if (Kc > W->K) Kc = W->K;
   pl.Kc = Kc;
   pl.KC = (W->K + Kc - 1) / Kc;
+  if (pl.KC > kMaxSlices) return CELTY_EINVAL;
   // the tile (int32) goes first: R rows, then 7 alignment rows and 128 rows
   // of slack that bound where a corrupt stream could write (base is capped at
   // R + 7 and a group adds at most 128)
@@ -482,7 +496,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   pl.scr_off = static_cast<int>(off);
   off += static_cast<size_t>(pl.waves) * kWave * 4;
   pl.misc_off = static_cast<int>(off);
-  off += static_cast<size_t>(4 * pl.waves + 2) * 4;
+  off += static_cast<size_t>(4 * pl.waves + 1) * 4;
   pl.lds = align_up(off, 16);
   if (pl.lds > static_cast<size_t>(kMaxLds)) return CELTY_EINVAL;
   pl.blocks = static_cast<int64_t>(W->T) * pl.KC;
@@ -508,9 +522,9 @@ celty_status launch(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
 
 extern "C" size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R) {
   (void)K;
-  if (M < 1 || R < 1) return 0;
-  const int64_t T = (static_cast<int64_t>(M) + R - 1) / R;
-  return align_up(static_cast<size_t>(M) * 4, 256) + align_up(static_cast<size_t>(T) * 4, 256);
+  (void)R;
+  if (M < 1) return 0;
+  return align_up(static_cast<size_t>(M) * 8, 256);
 }
 
 extern "C" celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
@@ -550,8 +564,18 @@ extern "C" celty_status celty_spmspv_ex(const celty_rlc_csc* W, const void* x, f
   a.runs = W->runs;
   a.x = static_cast<const unsigned short*>(x);
   a.y = static_cast<unsigned short*>(y);
-  a.ws = static_cast<float*>(workspace);
-  a.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + align_up(static_cast<size_t>(W->M) * 4, 256));
+  a.ws = static_cast<unsigned long long*>(workspace);
+  // merge scale: any row sum is at most K * max|w| * 65504 (the largest
+  // finite fp16 |x|); 2^s_glob maps that bound to at most 2^48
+  a.s_glob = 0;
+  {
+    const double bound = static_cast<double>(W->K) * static_cast<double>(W->max_abs) * 65504.0;
+    if (bound > 0.0) {
+      int e;
+      std::frexp(bound, &e);
+      a.s_glob = 48 - e;
+    }
+  }
   a.tau = tau;
   a.max_abs = W->max_abs;
   a.n_groups = static_cast<uint32_t>(W->n_groups);

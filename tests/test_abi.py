@@ -52,8 +52,9 @@ def test_status_strings():
 
 
 def test_workspace_bytes():
-    assert celty.celty_spmspv_workspace_bytes(4096, 4096, 256) == 4096 * 4 + 256
-    assert celty.celty_spmspv_workspace_bytes(1000, 7, 300) == 4096 + 256
+    # one 64-bit merge slot per output row, rounded to 256 bytes
+    assert celty.celty_spmspv_workspace_bytes(4096, 4096, 256) == 4096 * 8
+    assert celty.celty_spmspv_workspace_bytes(1000, 7, 300) == 8192
     assert celty.celty_spmspv_workspace_bytes(0, 1, 1) == 0
 
 
@@ -152,12 +153,20 @@ def test_spmspv_plan_is_host_only():
     assert celty._plan(ctypes.byref(d), ctypes.byref(bad), ctypes.byref(out), None, None) == CELTY_EINVAL
     big = _desc(M=100000, K=64, R=60000)                             # tile does not fit in LDS
     assert celty._plan(ctypes.byref(big), None, ctypes.byref(out), None, None) == CELTY_EINVAL
+    many = celty_launch(64, 4)                                       # 64 slices of 4096 columns > 63
+    assert celty._plan(ctypes.byref(d), ctypes.byref(many), ctypes.byref(out), None, None) == CELTY_EINVAL
+    ok = celty_launch(66, 4)                                         # 63 slices
+    assert celty._plan(ctypes.byref(d), ctypes.byref(ok), ctypes.byref(out), ctypes.byref(nb), None) == CELTY_OK
+    assert nb.value == d.T * 63
+    wide = _desc(K=200000)                                           # auto shape keeps <= 63 slices
+    assert celty._plan(ctypes.byref(wide), None, ctypes.byref(out), ctypes.byref(nb), None) == CELTY_OK
+    assert -(-200000 // out.cols_per_block) <= 63
 
 
 @host_only
 @pytest.mark.parametrize("case", ["null_desc", "version", "run_bits", "T", "values_align", "runs_align",
                                   "null_x", "nan_tau", "x_align", "overlap", "short_ws", "null_ws",
-                                  "ws_align", "waves", "max_abs_nan", "max_abs_inf", "max_abs_neg"])
+                                  "ws_align", "waves", "max_abs_nan", "max_abs_inf", "max_abs_neg", "slices"])
 def test_spmspv_rejects_bad_arguments(case):
     d = _desc()
     x, y, ws = FAKE + 0x100000, FAKE + 0x200000, FAKE + 0x300000
@@ -190,6 +199,8 @@ def test_spmspv_rejects_bad_arguments(case):
         ws += 16
     elif case == "waves":
         launch = celty_launch(64, 5)
+    elif case == "slices":
+        launch = celty_launch(32, 4)
     elif case == "max_abs_nan":
         d.max_abs = math.nan
     elif case == "max_abs_inf":

@@ -107,8 +107,8 @@ def test_spmspv_fuzz(celty, torch_dev, M, K, R, ws, as_):
     _check(y, p.W, p.mask, p.x, p.tau)
 
 
-@pytest.mark.parametrize("launch", [(1, 2), (17, 4), (64, 2), (64, 4), (128, 8), (256, 16), (1000, 4),
-                                    (4096, 4), (4096, 16)])
+@pytest.mark.parametrize("launch", [(40, 2), (41, 4), (64, 2), (64, 4), (128, 8), (256, 16), (1000, 4),
+                                    (4096, 4), (4096, 16), (700, 8)])
 def test_launch_shapes_agree(celty, torch_dev, launch):
     _note(f"launch shape {launch}")
     p = workloads.random_small(77, 3000, 2500, ws=60, as_=50)
