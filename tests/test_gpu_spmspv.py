@@ -198,7 +198,9 @@ def _full(celty, torch_dev, p, label):
     R = default_tile_rows(p.W.shape[0], p.W.shape[1])
     _note(f"full {label} M={p.W.shape[0]} K={p.W.shape[1]} R={R}")
     y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, R)
-    return _check(y, p.W, p.mask, p.x, p.tau)
+    err = _check(y, p.W, p.mask, p.x, p.tau)
+    _note(f"  rel_err={err:.3e}")
+    return err
 
 
 def test_config1(celty, torch_dev):
