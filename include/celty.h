@@ -145,6 +145,7 @@ celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int
 typedef struct celty_launch {
   int32_t cols_per_block;   /* columns of x one workgroup scans (1..4096) */
   int32_t waves_per_block;  /* 2, 4, 8 or 16 wavefronts of 64 lanes */
+  int32_t groups_per_lane;  /* 1, 2 or 4 eight-entry groups per lane per pass */
 } celty_launch;
 
 /* Bytes of device workspace celty_spmspv needs for this shape: one 64-bit
@@ -180,7 +181,7 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  * must bound every stored |value| (the encoder sets it).
  * Errors: EINVAL (null or misaligned pointers, inconsistent header, NaN tau,
  *         non-finite or negative max_abs, short workspace, more than 63
- *         column slices), EHIP.
+ *         column slices, 16 * n_groups >= 2^31), EHIP.
  */
 celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y,
                           void* workspace, size_t workspace_bytes, void* stream);

@@ -56,7 +56,7 @@ class celty_rlc_csc(ctypes.Structure):
 
 
 class celty_launch(ctypes.Structure):
-    _fields_ = [("cols_per_block", _i32), ("waves_per_block", _i32)]
+    _fields_ = [("cols_per_block", _i32), ("waves_per_block", _i32), ("groups_per_lane", _i32)]
 
 
 def _sig(name, res, *args):
@@ -257,8 +257,9 @@ def _launch_struct(launch) -> Optional[celty_launch]:
         return None
     if isinstance(launch, celty_launch):
         return launch
-    cols, waves = launch
-    return celty_launch(int(cols), int(waves))
+    cols, waves = launch[0], launch[1]
+    groups = launch[2] if len(launch) > 2 else 0
+    return celty_launch(int(cols), int(waves), int(groups))
 
 
 def celty_spmspv(W: DeviceRlcCsc, x, tau: float, y, workspace, stream=None) -> None:
@@ -283,7 +284,7 @@ def celty_spmspv_plan(W, launch=None) -> dict:
     _check(_plan(ctypes.byref(d), None if ls is None else ctypes.byref(ls), ctypes.byref(out),
                  ctypes.byref(nb), ctypes.byref(lds)), "celty_spmspv_plan")
     return dict(cols_per_block=out.cols_per_block, waves_per_block=out.waves_per_block,
-                blocks=nb.value, lds_bytes=lds.value)
+                groups_per_lane=out.groups_per_lane, blocks=nb.value, lds_bytes=lds.value)
 
 
 def default_tile_rows(M: int, K: int) -> int:

@@ -148,103 +148,169 @@ __device__ __forceinline__ int round_to_fixed(float v) {
   return r;
 }
 
-// One pass's input for a lane: its group of 8 entries and its segment.
-struct Pass {
-  uint4 v;           // 8 fp16 values
-  uint32_t rw;       // 8 packed 4-bit runs
-  int sid;           // segment (index into the workgroup's segment list)
-  int h;             // lane where the segment starts in this pass (<= 0: earlier)
-  uint32_t segend;   // flat end (exclusive) of the segment
-  float xs;          // scaled x_k of the segment's column
-  bool live;         // the lane holds a group
+// Buffer resources for the values and runs arrays: 32-bit offsets, and the
+// hardware returns zeros for any read past num_records, so a corrupt
+// group-pointer array cannot read outside the arrays.
+struct Streams {
+  __amdgpu_buffer_rsrc_t values;
+  __amdgpu_buffer_rsrc_t runs;
 };
 
-// Assigns the 64 groups starting at flat position pb to lanes and issues
-// their loads.  icur is the segment holding group pb.  A pass at or past the
-// end (pb >= pe) skips the assignment and has every lane idle.
-template <class Args>
-__device__ __forceinline__ Pass fetch_pass(const Args& p, const SegInfo* seg, int* scr, uint32_t pb, int icur,
-                                           int i_end, uint32_t pe, int lane) {
-  Pass a;
-  a.sid = icur;
-  a.h = 0;
-  a.segend = pe;
-  a.xs = 0.f;
-  a.live = false;
-  uint32_t gl = 0u;
+__device__ __forceinline__ Streams make_streams(const uint4* values, const uint32_t* runs, uint32_t n_groups) {
+  Streams st;
+  st.values = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(values), static_cast<short>(0),
+                                                static_cast<int>(n_groups * 16u), 0x00020000);
+  st.runs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(runs), static_cast<short>(0),
+                                              static_cast<int>(n_groups * 4u), 0x00020000);
+  return st;
+}
+
+// One pass's input for a lane: G consecutive groups of the workgroup's flat
+// sequence (8 entries each) and, per group, its segment's head and x.
+template <int G>
+struct Pass {
+  uint4 v[G];        // 8 fp16 values per group
+  uint32_t rw[G];    // 8 packed 4-bit runs per group
+  int hpos[G];       // flat position of the group's segment head relative to the pass start (< 0: earlier)
+  float xs[G];       // scaled x_k of the group's column
+  uint32_t live;     // bit i: group i holds data
+  int sid63;         // segment of lane 63's last group (wavefront-uniform)
+  uint32_t end63;    // its flat end (wavefront-uniform)
+};
+
+// Assigns the 64*G groups starting at flat position pb to lanes (lane l takes
+// groups pb + G*l .. pb + G*l + G-1) and issues their loads.  icur is the
+// segment holding group pb.  A pass at or past the end (pb >= pe) skips the
+// assignment and has every lane idle.  scr holds 64*G ints per wavefront:
+// segment heads are tagged with a negative value unique to the pass (the
+// accumulation step stores non-negative prefix sums in the same array).
+template <int G>
+__device__ __forceinline__ void fetch_pass(Pass<G>& a, const Streams& st, const SegInfo* seg, int* scr,
+                                           uint32_t pb, int icur, int i_end, uint32_t pe, int lane) {
+  constexpr uint32_t P = kWave * G;
+  a.live = 0u;
+  a.sid63 = icur;
+  a.end63 = pe;
+  uint32_t gl[G];
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    a.hpos[i] = 0;
+    a.xs[i] = 0.f;
+    gl[i] = 0u;
+  }
   if (pb < pe) {   // wavefront-uniform
-    // heads of the segments that start inside (pb, pb + 64): tag their lane
-    const int j = icur + lane;
-    if (lane > 0 && j < i_end) {
-      const uint32_t o = seg[j].off;
-      if (o < pb + kWave) scr[o - pb] = static_cast<int>(pb + 1u);
+    const int tag = -static_cast<int>(pb) - 1;
+    // segments icur+1 .. icur+64G are the only ones that can start in the pass
+#pragma unroll
+    for (int m = 0; m < G; ++m) {
+      const int j = icur + 1 + lane + kWave * m;
+      if (j < i_end) {
+        const uint32_t o = seg[j].off;
+        if (o < pb + P) scr[o - pb] = tag;
+      }
     }
     wave_lds_sync();
-    const bool head = lane > 0 && scr[lane] == static_cast<int>(pb + 1u);
-    const uint64_t hm = __ballot(head);
-    a.sid = min(icur + static_cast<int>(lanes_below(hm)) + (head ? 1 : 0), i_end - 1);
-    const SegInfo si = seg[a.sid];
-    const uint32_t f = pb + static_cast<uint32_t>(lane);
-    a.live = f < pe;
-    a.h = static_cast<int>(si.off) - static_cast<int>(pb);
-    a.segend = si.off + si.cnt;
-    a.xs = si.xs;
-    // gi < n_groups always holds for an encoder-made stream; the test keeps a
-    // corrupt group-pointer array from reading outside the arrays
-    const uint32_t gi = si.gstart + (f - si.off);
-    gl = (a.live && gi < p.n_groups) ? gi : 0u;
+    uint32_t fl = 0u;   // bit i: position G*lane + i is a segment head
+#pragma unroll
+    for (int i = 0; i < G; ++i) fl |= (scr[G * lane + i] == tag ? 1u : 0u) << i;
+    const uint32_t nh = __popc(fl);
+    // heads in the positions of the lanes below, from the bits of nh
+    int cum = 0;
+#pragma unroll
+    for (int b = 0; (1 << b) <= G; ++b) cum += static_cast<int>(lanes_below(__ballot((nh >> b) & 1u))) << b;
+    int sid = icur;
+    uint32_t end = pe;
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      cum += (fl >> i) & 1u;
+      sid = min(icur + cum, i_end - 1);
+      const SegInfo si = seg[sid];
+      const uint32_t f = pb + static_cast<uint32_t>(G * lane + i);
+      const bool lv = f < pe;
+      a.hpos[i] = static_cast<int>(si.off) - static_cast<int>(pb);
+      a.xs[i] = si.xs;
+      gl[i] = lv ? si.gstart + (f - si.off) : 0u;
+      a.live |= (lv ? 1u : 0u) << i;
+      end = si.off + si.cnt;
+    }
+    a.sid63 = __builtin_amdgcn_readlane(sid, kWave - 1);
+    a.end63 = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(end), kWave - 1));
   }
   // Loads are issued by every lane of every pass (idle lanes and idle passes
   // read group 0 and drop it), so the wait for one pass's data can leave the
   // later passes' loads in flight.
-  a.v = p.values[gl];
-  a.rw = p.runs[gl];
-  return a;
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(st.values, static_cast<int>(gl[i] << 4), 0, 0);
+    a.v[i] = make_uint4(v[0], v[1], v[2], v[3]);
+    a.rw[i] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>(gl[i] << 2), 0, 0);
+  }
 }
 
 // The segment holding the first group of the pass after the one fetched at
 // flat position pb (wavefront-uniform).
-__device__ __forceinline__ int next_pass_segment(const Pass& a, uint32_t pb, int i_end) {
-  const int sid63 = __builtin_amdgcn_readlane(a.sid, kWave - 1);
-  const uint32_t end63 = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(a.segend), kWave - 1));
-  return min(end63 > pb + kWave ? sid63 : sid63 + 1, i_end - 1);
+template <int G>
+__device__ __forceinline__ int next_pass_segment(const Pass<G>& a, uint32_t pb, int i_end) {
+  return min(a.end63 > pb + kWave * G ? a.sid63 : a.sid63 + 1, i_end - 1);
 }
 
-// Decodes one pass and adds its products into the fixed-point tile.  Returns,
-// per lane, the segment-relative sum of (run + 1) through the lane's group
-// (the carry when the segment goes on into the next pass).
-__device__ __forceinline__ int accumulate_pass(int* tile, const Pass& a, int carry, int base_cap, bool idle) {
-  if (idle) return 0;   // wavefront-uniform
-  // byte k of O: inclusive prefix of (run + 1) through entry 2k+1; byte k of
-  // E: the same through entry 2k.  The byte-wise running sum is two shift-adds
-  // (kept as such rather than the quarter-rate multiply by 0x01010101).
-  const uint32_t rw = a.live ? a.rw : 0u;
-  const uint32_t r_even = rw & 0x0F0F0F0Fu;
-  const uint32_t r_odd = (rw >> 4) & 0x0F0F0F0Fu;
-  const uint32_t pair = r_even + r_odd + 0x02020202u;
-  uint32_t half, O;
-  asm("v_lshl_add_u32 %0, %1, 8, %1" : "=v"(half) : "v"(pair));
-  asm("v_lshl_add_u32 %0, %1, 16, %1" : "=v"(O) : "v"(half));
-  const uint32_t E = O - r_odd - 0x01010101u;
-  const int S = a.live ? static_cast<int>(O >> 24) : 0;   // lane total
-  const int incl = wave_inclusive_scan(S);
-  const int excl = incl - S;
-  const int eh = __builtin_amdgcn_ds_bpermute((a.h > 0 ? a.h : 0) << 2, excl);
-  const int rel = excl - eh + (a.h < 0 ? carry : 0);     // segment-relative
-  if (a.live) {
+// Decodes one pass and adds its products into the fixed-point tile.  Returns
+// the segment-relative sum of (run + 1) through lane 63's last group (the
+// carry when that segment goes on into the next pass), wavefront-uniform.
+template <int G>
+__device__ __forceinline__ int accumulate_pass(int* tile, const Pass<G>& a, int carry, int base_cap, int* scr,
+                                               int lane) {
+  uint32_t E[G], O[G];
+  int S[G], C[G];
+  int T = 0;
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    // byte k of O: inclusive prefix of (run + 1) through entry 2k+1; byte k
+    // of E: the same through entry 2k.  The byte-wise running sum is two
+    // shift-adds (kept as such rather than the quarter-rate multiply by
+    // 0x01010101).
+    const bool lv = (a.live >> i) & 1u;
+    const uint32_t rw = lv ? a.rw[i] : 0u;
+    const uint32_t r_even = rw & 0x0F0F0F0Fu;
+    const uint32_t r_odd = (rw >> 4) & 0x0F0F0F0Fu;
+    const uint32_t pair = r_even + r_odd + 0x02020202u;
+    uint32_t half, o;
+    asm("v_lshl_add_u32 %0, %1, 8, %1" : "=v"(half) : "v"(pair));
+    asm("v_lshl_add_u32 %0, %1, 16, %1" : "=v"(o) : "v"(half));
+    O[i] = o;
+    E[i] = o - r_odd - 0x01010101u;
+    S[i] = lv ? static_cast<int>(o >> 24) : 0;   // the group's total
+    C[i] = T;                                     // before the group, within the lane
+    T += S[i];
+  }
+  const int incl = wave_inclusive_scan(T);
+  const int X = incl - T;   // before the lane's first group, within the pass
+  // prefix sum before every flat position of the pass, for the segment heads
+#pragma unroll
+  for (int i = 0; i < G; ++i) scr[G * lane + i] = X + C[i];
+  wave_lds_sync();
+  int tail = 0;
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    const int Y = X + C[i];
+    const int at_head = scr[max(a.hpos[i], 0)];
+    const int rel = a.hpos[i] >= 0 ? Y - at_head : Y + carry;   // segment-relative
     // row of entry j = base + prefix_j; base >= -1 and prefix_j <= 128, and the
     // cap keeps even a corrupt stream inside the tile's slack
     const int base = min(rel - 1, base_cap);
-    const uint32_t w4[4] = {a.v.x, a.v.y, a.v.z, a.v.w};
+    if ((a.live >> i) & 1u) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int re = base + static_cast<int>((E >> (8 * q)) & 0xFFu);
-      const int ro = base + static_cast<int>((O >> (8 * q)) & 0xFFu);
-      atomicAdd(tile + re, round_to_fixed(mul_lo_f16(w4[q], a.xs)));
-      atomicAdd(tile + ro, round_to_fixed(mul_hi_f16(w4[q], a.xs)));
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t w = q == 0 ? a.v[i].x : q == 1 ? a.v[i].y : q == 2 ? a.v[i].z : a.v[i].w;
+        const int re = base + static_cast<int>((E[i] >> (8 * q)) & 0xFFu);
+        const int ro = base + static_cast<int>((O[i] >> (8 * q)) & 0xFFu);
+        atomicAdd(tile + re, round_to_fixed(mul_lo_f16(w, a.xs[i])));
+        atomicAdd(tile + ro, round_to_fixed(mul_hi_f16(w, a.xs[i])));
+      }
     }
+    if (i == G - 1) tail = rel + S[i];
   }
-  return rel + S;
+  return __builtin_amdgcn_readlane(tail, kWave - 1);
 }
 
 struct KernelArgs {
@@ -262,7 +328,7 @@ struct KernelArgs {
   int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS (the tile is at 0)
 };
 
-template <int WAVES, int DEPTH = 3>
+template <int WAVES, int G, int DEPTH>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   constexpr int NT = WAVES * kWave;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -279,7 +345,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   const int base_cap = p.R + 7;
 
   for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0;
-  scr_all[tid] = 0;
+  for (int i = tid; i < NT * G; i += NT) scr_all[i] = 0;
 
   // ---- selection of this slice's active, non-empty columns ----------------
   const int k0 = c * p.Kc;
@@ -336,40 +402,42 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   if (n_seg == 0 && tid <= WAVES) wfirst[tid] = 0;
   __syncthreads();
 
-  // ---- per-wavefront walk over 64-group passes ----------------------------
+  // ---- per-wavefront walk over passes of 64*G groups -----------------------
   // A ring of DEPTH passes is kept in flight: after a pass is decoded and
   // accumulated, its slot is refilled with the loads of the pass DEPTH ahead.
   // The ring is indexed by compile-time constants (fully unrolled), so no
   // register copies force an early wait.  Passes past the end are idle (every
   // lane inactive, loads of group 0) and accumulate nothing.
+  constexpr uint32_t P = kWave * G;
   const int i_begin = wfirst[wv], i_end = wfirst[wv + 1];
   if (i_begin < i_end) {
-    int* scr = scr_all + wv * kWave;
+    const Streams st = make_streams(p.values, p.runs, p.n_groups);
+    int* scr = scr_all + wv * kWave * G;
     const uint32_t pb0 = seg[i_begin].off;
     const uint32_t pe = i_end < static_cast<int>(n_seg) ? seg[i_end].off : n_grp;
-    const int n_pass = static_cast<int>((pe - pb0 + kWave - 1) / kWave);
-    Pass ring[DEPTH];
+    const int n_pass = static_cast<int>((pe - pb0 + P - 1) / P);
+    Pass<G> ring[DEPTH];
     uint32_t pf = pb0;    // flat start of the next pass to fetch
     int icur = i_begin;   // segment holding group pf
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) {
-      ring[d] = fetch_pass(p, seg, scr, pf, icur, i_end, pe, lane);
-      icur = next_pass_segment(ring[d], pf, i_end);
-      pf += kWave;
+      fetch_pass<G>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
+      icur = next_pass_segment<G>(ring[d], pf, i_end);
+      pf += P;
     }
     uint32_t pb = pb0;    // flat start of the pass being accumulated
     int carry = 0;        // sum of (run + 1) over its first segment's earlier groups
     for (int done = 0; done < n_pass; done += DEPTH) {
 #pragma unroll
       for (int d = 0; d < DEPTH; ++d) {
-        const int tail = accumulate_pass(tile, ring[d], carry, base_cap, pb >= pe);
-        const uint32_t end63 =
-            static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(ring[d].segend), kWave - 1));
-        carry = end63 > pb + kWave ? __builtin_amdgcn_readlane(tail, kWave - 1) : 0;
-        pb += kWave;
-        ring[d] = fetch_pass(p, seg, scr, pf, icur, i_end, pe, lane);
-        icur = next_pass_segment(ring[d], pf, i_end);
-        pf += kWave;
+        if (pb < pe) {   // wavefront-uniform
+          const int tail = accumulate_pass<G>(tile, ring[d], carry, base_cap, scr, lane);
+          carry = ring[d].end63 > pb + P ? tail : 0;
+        }
+        pb += P;
+        fetch_pass<G>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
+        icur = next_pass_segment<G>(ring[d], pf, i_end);
+        pf += P;
       }
     }
   }
@@ -447,7 +515,7 @@ __global__ __launch_bounds__(1024) void select_kernel(const unsigned short* __re
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Plan {
-  int waves = 4, Kc = 0, KC = 0, T = 0, tile_slots = 0;
+  int waves = 4, groups = 1, Kc = 0, KC = 0, T = 0, tile_slots = 0;
   int seg_off = 0, scr_off = 0, misc_off = 0;
   int64_t blocks = 0;
   size_t lds = 0;
@@ -462,6 +530,8 @@ celty_status check_header(const celty_rlc_csc* W) {
   if (W->T != static_cast<int32_t>((static_cast<int64_t>(W->M) + W->R - 1) / W->R)) return CELTY_EINVAL;
   if (W->n_groups < 0 || W->n_groups > static_cast<int64_t>(UINT32_MAX)) return CELTY_EINVAL;
   if (!W->gptr || misaligned(W->gptr, 4)) return CELTY_EINVAL;
+  // buffer resources take byte sizes below 2^31
+  if (W->n_groups * 16 > static_cast<int64_t>(INT32_MAX)) return CELTY_EINVAL;
   if (W->n_groups > 0 && (!W->values || !W->runs)) return CELTY_EINVAL;
   if (!(W->max_abs >= 0.f) || std::isinf(W->max_abs)) return CELTY_EINVAL;
   if (misaligned(W->values, 16) || misaligned(W->runs, 4)) return CELTY_EINVAL;
@@ -486,6 +556,16 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   pl.Kc = Kc;
   pl.KC = (W->K + Kc - 1) / Kc;
   if (pl.KC > kMaxSlices) return CELTY_EINVAL;
+  pl.groups = cfg ? cfg->groups_per_lane : 0;
+  if (pl.groups == 0) {
+    // groups per lane per pass: enough passes per wavefront to keep them
+    // busy, as few as possible to amortise the per-pass bookkeeping
+    // (entries per wavefront estimated at half the columns active)
+    const double density = static_cast<double>(W->n_entries) / (static_cast<double>(W->M) * W->K);
+    const double per_wave = 0.5 * Kc * static_cast<double>(W->R) * density / pl.waves;
+    pl.groups = per_wave >= 4 * 2048.0 ? 4 : per_wave >= 4 * 1024.0 ? 2 : 1;
+  }
+  if (pl.groups != 1 && pl.groups != 2 && pl.groups != 4) return CELTY_EINVAL;
   // the tile (int32) goes first: R rows, then 7 alignment rows and 128 rows
   // of slack that bound where a corrupt stream could write (base is capped at
   // R + 7 and a group adds at most 128)
@@ -494,7 +574,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   pl.seg_off = static_cast<int>(off);
   off += static_cast<size_t>(Kc) * sizeof(SegInfo);
   pl.scr_off = static_cast<int>(off);
-  off += static_cast<size_t>(pl.waves) * kWave * 4;
+  off += static_cast<size_t>(pl.waves) * kWave * pl.groups * 4;
   pl.misc_off = static_cast<int>(off);
   off += static_cast<size_t>(4 * pl.waves + 1) * 4;
   pl.lds = align_up(off, 16);
@@ -504,18 +584,28 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   return CELTY_OK;
 }
 
-template <int WAVES>
-celty_status launch(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
+template <int WAVES, int G, int DEPTH>
+celty_status launch_shape(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
   static bool attr_set = false;
   if (pl.lds > 64 * 1024 && !attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&spmspv_kernel<WAVES>),
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&spmspv_kernel<WAVES, G, DEPTH>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds) != hipSuccess)
       return CELTY_EHIP;
     attr_set = true;
   }
-  hipLaunchKernelGGL(spmspv_kernel<WAVES>, dim3(static_cast<unsigned>(pl.blocks)), dim3(WAVES * kWave),
+  hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(pl.blocks)), dim3(WAVES * kWave),
                      pl.lds, stream, a);
   return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
+}
+
+template <int WAVES>
+celty_status launch(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
+  switch (pl.groups) {
+    case 1: return launch_shape<WAVES, 1, 3>(pl, a, stream);
+    case 2: return launch_shape<WAVES, 2, 2>(pl, a, stream);
+    case 4: return launch_shape<WAVES, 4, 2>(pl, a, stream);
+    default: return CELTY_EINVAL;
+  }
 }
 
 }  // namespace
@@ -541,6 +631,7 @@ extern "C" celty_status celty_spmspv_plan(const celty_rlc_csc* W, const celty_la
   if (celty_status st = make_plan(W, launch_cfg, pl)) return st;
   resolved->cols_per_block = pl.Kc;
   resolved->waves_per_block = pl.waves;
+  resolved->groups_per_lane = pl.groups;
   if (n_blocks) *n_blocks = pl.blocks;
   if (lds_bytes) *lds_bytes = static_cast<int64_t>(pl.lds);
   return CELTY_OK;

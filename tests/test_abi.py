@@ -145,8 +145,11 @@ def test_spmspv_plan_is_host_only():
     out, nb, lds = celty_launch(), ctypes.c_int64(), ctypes.c_int64()
     assert celty._plan(ctypes.byref(d), None, ctypes.byref(out), ctypes.byref(nb), ctypes.byref(lds)) == CELTY_OK
     assert out.waves_per_block in (2, 4, 8, 16) and 1 <= out.cols_per_block <= 4096
+    assert out.groups_per_lane in (1, 2, 4)
     assert nb.value == d.T * (-(-d.K // out.cols_per_block))
     assert 0 < lds.value <= 160 * 1024
+    bad = celty_launch(66, 4, 3)                                      # groups per lane
+    assert celty._plan(ctypes.byref(d), ctypes.byref(bad), ctypes.byref(out), None, None) == CELTY_EINVAL
     bad = celty_launch(64, 3)
     assert celty._plan(ctypes.byref(d), ctypes.byref(bad), ctypes.byref(out), None, None) == CELTY_EINVAL
     bad = celty_launch(5000, 4)

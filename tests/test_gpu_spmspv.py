@@ -100,15 +100,17 @@ FUZZ = [(1, 1, 1), (1, 5, 8), (5, 1, 8), (3, 200, 1), (100, 100, 16), (257, 129,
 
 @pytest.mark.parametrize("M,K,R", FUZZ)
 @pytest.mark.parametrize("ws,as_", [(0, 0), (50, 50), (90, 30), (30, 90)])
-def test_spmspv_fuzz(celty, torch_dev, M, K, R, ws, as_):
-    _note(f"fuzz M={M} K={K} R={R} ws={ws} as={as_}")
+@pytest.mark.parametrize("groups", [1, 4])
+def test_spmspv_fuzz(celty, torch_dev, M, K, R, ws, as_, groups):
+    _note(f"fuzz M={M} K={K} R={R} ws={ws} as={as_} groups={groups}")
     p = workloads.random_small(M * 13 + K * 7 + R + ws, M, K, ws=ws, as_=as_, zero_weights=3)
-    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, R)
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, R, launch=(0, 0, groups))
     _check(y, p.W, p.mask, p.x, p.tau)
 
 
-@pytest.mark.parametrize("launch", [(40, 2), (41, 4), (64, 2), (64, 4), (128, 8), (256, 16), (1000, 4),
-                                    (4096, 4), (4096, 16), (700, 8)])
+@pytest.mark.parametrize("launch", [(40, 2, 1), (41, 4, 2), (64, 2, 4), (64, 4, 1), (128, 8, 2), (256, 16, 4),
+                                    (1000, 4, 1), (1000, 4, 4), (4096, 4, 2), (4096, 16, 1), (700, 8, 4),
+                                    (2500, 2, 4)])
 def test_launch_shapes_agree(celty, torch_dev, launch):
     _note(f"launch shape {launch}")
     p = workloads.random_small(77, 3000, 2500, ws=60, as_=50)
