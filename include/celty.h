@@ -141,7 +141,8 @@ celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int
 
 /* Launch shape of celty_spmspv_ex.  Zero fields mean "choose automatically".
  * The K columns are cut into ceil(K / cols_per_block) slices, at most 63
- * (the merge counts slices in one byte of a 64-bit word). */
+ * (the merge counts slices in one byte of a 64-bit word).  A workgroup's
+ * lanes scan at most 8 columns each: cols_per_block <= 512 * waves_per_block. */
 typedef struct celty_launch {
   int32_t cols_per_block;   /* columns of x one workgroup scans (1..4096) */
   int32_t waves_per_block;  /* 2, 4, 8 or 16 wavefronts of 64 lanes */
@@ -181,7 +182,8 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  * must bound every stored |value| (the encoder sets it).
  * Errors: EINVAL (null or misaligned pointers, inconsistent header, NaN tau,
  *         non-finite or negative max_abs, short workspace, more than 63
- *         column slices, 16 * n_groups >= 2^31), EHIP.
+ *         column slices, cols_per_block above 512 * waves_per_block,
+ *         16 * n_groups >= 2^31), EHIP.
  */
 celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y,
                           void* workspace, size_t workspace_bytes, void* stream);

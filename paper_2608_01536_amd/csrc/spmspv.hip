@@ -2,18 +2,18 @@
 //
 // One launch computes y = W x_A (Sections 3.1-3.3):
 //   * grid = (row tile t) x (slice c of x).  A workgroup selects the active
-//     columns of its slice (|x_k| > tau, wavefront ballot + prefix sums:
-//     Section 3.1's column skip turned into stream compaction) and drops
-//     columns whose segment in tile t is empty;
+//     columns of its slice (|x_k| > tau; one block-wide scan of per-lane
+//     counts: Section 3.1's column skip turned into stream compaction) and
+//     drops columns whose segment in tile t is empty;
 //   * the workgroup's compressed groups (8 entries = 16 B of fp16 values +
 //     4 B of packed 4-bit runs) form one flat sequence; it is cut at segment
 //     boundaries into one contiguous range per wavefront;
-//   * a wavefront walks its range 64 groups (512 entries) per pass, keeping a
-//     ring of passes in flight: each lane loads one group with a 128-bit and a
-//     32-bit load (Section 3.1), turns the 8 runs into 8 inclusive prefixes
-//     with byte-packed arithmetic, and combines lanes with a wavefront scan
-//     that restarts at segment heads (Algorithm 1: prefix of runs plus
-//     ordinal gives the row);
+//   * a wavefront walks its range 64*G groups per pass, keeping a ring of
+//     passes in flight: each lane loads its groups with 128-bit and 32-bit
+//     buffer loads (Section 3.1), turns the 8 runs of a group into 8
+//     inclusive prefixes with byte-packed arithmetic, and combines lanes with
+//     a wavefront scan that restarts at segment heads (Algorithm 1: prefix of
+//     runs plus ordinal gives the row);
 //   * each product value * x_k is exact in fp32 (two fp16 factors) and is
 //     added into an LDS tile of the R output rows (Section 3.3's
 //     scatter-accumulation in on-chip memory).  The tile holds int32 fixed
@@ -22,14 +22,15 @@
 //     small fraction of an fp32 one, and the rounding error of a row,
 //     n^2 * max|w x| * 2^-32 for n active columns in the slice, stays below
 //     the worst case of fp32 accumulation;
-//   * the tile is merged across slices with fp32 atomics into a workspace row
-//     block; the last workgroup of a row tile (counter) writes y in fp16 and
-//     clears its workspace rows and counter for the next call.  With a single
-//     slice the tile goes straight to y.
+//   * the slices of a row tile are merged with one returning 64-bit atomic
+//     per row (fixed point at a launch-wide scale plus an arrival count); the
+//     slice that arrives last writes y[row] in fp16 and clears the slot for
+//     the next call.  With a single slice the tile goes straight to y.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <climits>
 #include <cmath>
 #include <cstdint>
 
@@ -41,6 +42,7 @@ constexpr int kWave = 64;
 constexpr int kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kSlack = 8 + 128;       // tile rows past R: alignment entries, and the cap's reach
 constexpr int kMaxSlices = 63;        // column slices per row tile (merge ticket count byte)
+constexpr int kMaxCols = 8;           // columns per thread in the selection
 
 struct SegInfo {
   uint32_t gstart;   // first group of the segment in the values/runs arrays
@@ -93,39 +95,79 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-// Block-wide: exclusive scans of a and b, their totals, and the maximum of m.
-// part[] holds 3*WAVES words.
+// Inclusive scan / suffix minimum over the 16 lanes of each DPP row.
+__device__ __forceinline__ uint32_t row_inclusive_scan(uint32_t v) {
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false));
+  return v;
+}
+__device__ __forceinline__ uint32_t row_inclusive_max(uint32_t v) {
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false)));
+  return v;
+}
+__device__ __forceinline__ int row_suffix_min(int v) {   // lanes past the row end count as INT_MAX
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x101, 0xF, 0xF, false));   // row_shl:1
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x102, 0xF, 0xF, false));   // row_shl:2
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x104, 0xF, 0xF, false));   // row_shl:4
+  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x108, 0xF, 0xF, false));   // row_shl:8
+  return v;
+}
+
+// Block-wide: exclusive scans of a and b, their totals, and the maximum of m
+// (WAVES <= 16).  Each wavefront's totals go to part[] (3*WAVES words, used
+// once per launch); after the barrier lane l < WAVES of every wavefront reads
+// wavefront l's totals and one row scan gives the offsets of all wavefronts.
 template <int WAVES>
 __device__ __forceinline__ void block_scan_select(uint32_t a, uint32_t b, uint32_t m, uint32_t& ea, uint32_t& eb,
                                                   uint32_t& ta, uint32_t& tb, uint32_t& tm, uint32_t* part) {
-  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-  const int ia = wave_inclusive_scan(static_cast<int>(a));
-  const int ib = wave_inclusive_scan(static_cast<int>(b));
+  static_assert(WAVES <= 16, "one DPP row holds the per-wavefront totals");
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+  const uint32_t ia = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(a)));
+  const uint32_t ib = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(b)));
   const uint32_t im = wave_inclusive_max(m);
   if (lane == kWave - 1) {
-    part[wv] = static_cast<uint32_t>(ia);
-    part[WAVES + wv] = static_cast<uint32_t>(ib);
+    part[wv] = ia;
+    part[WAVES + wv] = ib;
     part[2 * WAVES + wv] = im;
   }
   __syncthreads();
-  uint32_t oa = 0, ob = 0, sa = 0, sb = 0, mm = 0;
-#pragma unroll
-  for (int w = 0; w < WAVES; ++w) {
-    const uint32_t pa = part[w], pb = part[WAVES + w];
-    if (w < wv) {
-      oa += pa;
-      ob += pb;
-    }
-    sa += pa;
-    sb += pb;
-    mm = max(mm, part[2 * WAVES + w]);
+  uint32_t pa = 0, pb = 0, pm = 0;
+  if (lane < WAVES) {
+    pa = part[lane];
+    pb = part[WAVES + lane];
+    pm = part[2 * WAVES + lane];
   }
-  ea = oa + static_cast<uint32_t>(ia) - a;
-  eb = ob + static_cast<uint32_t>(ib) - b;
-  ta = sa;
-  tb = sb;
-  tm = mm;
-  __syncthreads();
+  const uint32_t sa = row_inclusive_scan(pa), sb = row_inclusive_scan(pb), sm = row_inclusive_max(pm);
+  ta = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sa), WAVES - 1));
+  tb = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sb), WAVES - 1));
+  tm = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sm), WAVES - 1));
+  const uint32_t oa = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sa - pa), wv));
+  const uint32_t ob = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sb - pb), wv));
+  ea = oa + ia - a;
+  eb = ob + ib - b;
+}
+
+// Fixed-point scale of a slice: a row sums at most n_seg terms, each at most
+// max|w| * max|x| in magnitude; 2^s puts that bound at or below 2^30.
+__device__ __forceinline__ int fixed_point_scale(uint32_t n_seg, float max_abs, uint32_t xmax_bits) {
+  const float bound = static_cast<float>(n_seg) * max_abs * __uint_as_float(xmax_bits);
+  if (!(bound > 0.f)) return 0;
+  int e;
+  frexpf(bound, &e);   // bound < 2^e
+  return min(max(30 - e, -64), 64);
+}
+
+// Wavefront of a segment starting at flat group offset off: non-decreasing in
+// off (rounding included), in [0, WAVES).
+template <int WAVES>
+__device__ __forceinline__ int wave_of(uint32_t off, float wscale) {
+  return min(static_cast<int>(static_cast<float>(off) * wscale), WAVES - 1);
 }
 
 // fp16 (low or high half of a word) times an fp32 value, in one mixed-precision
@@ -336,7 +378,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   SegInfo* seg = reinterpret_cast<SegInfo*>(smem + p.seg_off);
   int* scr_all = reinterpret_cast<int*>(smem + p.scr_off);
   uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 3*WAVES
-  int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES+1
+  int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int t = blockIdx.x / p.KC, c = blockIdx.x - t * p.KC;
@@ -346,60 +388,79 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
 
   for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0;
   for (int i = tid; i < NT * G; i += NT) scr_all[i] = 0;
+  if (tid < WAVES) wfirst[tid] = INT_MAX;
+  int scale = 0;   // the workgroup's fixed-point scale 2^scale
 
   // ---- selection of this slice's active, non-empty columns ----------------
+  // The flat group sequence is then cut into one range per wavefront:
+  // segment i goes to wavefront wave_of(off_i), and wfirst[w] collects the
+  // lowest segment index of wavefront w (INT_MAX when none starts there).
   const int k0 = c * p.Kc;
   const int kn = min(p.Kc, p.K - k0);
   const uint32_t* gp = p.gptr + static_cast<size_t>(t) * p.K + k0;
-  uint32_t n_seg = 0, n_grp = 0, xmax_bits = 0;
-  for (int it = 0; it < kn; it += NT) {
-    const int kk = it + tid;
-    uint32_t g0 = 0, g1 = 0;
-    float xv = 0.f;
-    bool keep = false;
-    if (kk < kn) {
-      xv = half_bits_to_float(p.x[k0 + kk]);
-      g0 = gp[kk];
-      g1 = gp[kk + 1];
-      keep = (fabsf(xv) > p.tau) && (g1 > g0);
+  uint32_t n_seg, n_grp;
+  if (kn <= NT) {
+    // one column per lane
+    uint32_t g0 = 0u, g1 = 0u, xr = 0u;
+    if (tid < kn) {
+      g0 = gp[tid];
+      g1 = gp[tid + 1];
+      xr = p.x[k0 + tid];
     }
+    const float xv = half_bits_to_float(xr);
+    const bool keep = tid < kn && fabsf(xv) > p.tau && g1 > g0;
     const uint32_t cnt = keep ? g1 - g0 : 0u;
     // |x| >= 0 orders like its bit pattern
-    const uint32_t mbits = keep ? __float_as_uint(fabsf(xv)) : 0u;
-    uint32_t en, eg, tn, tg, tm;
-    block_scan_select<WAVES>(keep ? 1u : 0u, cnt, mbits, en, eg, tn, tg, tm, part);
-    // x_k is stored unscaled for now; the scale is known after the last step
-    if (keep) seg[n_seg + en] = SegInfo{g0, n_grp + eg, cnt, xv};
-    n_seg += tn;
-    n_grp += tg;
-    xmax_bits = max(xmax_bits, tm);
+    uint32_t en, eg, xmax_bits;
+    block_scan_select<WAVES>(keep ? 1u : 0u, cnt, keep ? __float_as_uint(fabsf(xv)) : 0u, en, eg, n_seg, n_grp,
+                             xmax_bits, part);
+    const int s = fixed_point_scale(n_seg, p.max_abs, xmax_bits);
+    const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
+    if (keep) {
+      seg[en] = SegInfo{g0, eg, cnt, ldexpf(xv, s)};
+      atomicMin(wfirst + wave_of<WAVES>(eg, wscale), static_cast<int>(en));
+    }
+    scale = s;
+  } else {
+    // m <= kMaxCols consecutive columns per lane, so one block scan still
+    // orders all of them: segment order is column order
+    const int m = (kn + NT - 1) / NT;
+    const int kb = tid * m;
+    // all kMaxCols slots are loaded, at clamped indices and without branches,
+    // so that no load waits for another; columns at or past kn, or past the
+    // lane's m, are dropped by the keep test
+    uint32_t g[kMaxCols + 1], xr[kMaxCols];
+#pragma unroll
+    for (int j = 0; j <= kMaxCols; ++j) g[j] = gp[min(kb + j, kn)];
+#pragma unroll
+    for (int j = 0; j < kMaxCols; ++j) xr[j] = p.x[k0 + min(kb + j, kn - 1)];
+    uint32_t keep_bits = 0u, n_loc = 0u, g_loc = 0u, m_loc = 0u;
+#pragma unroll
+    for (int j = 0; j < kMaxCols; ++j) {
+      const float xv = half_bits_to_float(xr[j]);
+      const bool keep = j < m && kb + j < kn && fabsf(xv) > p.tau && g[j + 1] > g[j];
+      keep_bits |= (keep ? 1u : 0u) << j;
+      n_loc += keep ? 1u : 0u;
+      g_loc += keep ? g[j + 1] - g[j] : 0u;
+      m_loc = max(m_loc, keep ? __float_as_uint(fabsf(xv)) : 0u);
+    }
+    uint32_t en, eg, xmax_bits;
+    block_scan_select<WAVES>(n_loc, g_loc, m_loc, en, eg, n_seg, n_grp, xmax_bits, part);
+    const int s = fixed_point_scale(n_seg, p.max_abs, xmax_bits);
+    const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
+    uint32_t idx = en, off = eg;
+#pragma unroll
+    for (int j = 0; j < kMaxCols; ++j) {
+      if ((keep_bits >> j) & 1u) {
+        const uint32_t cnt = g[j + 1] - g[j];
+        seg[idx] = SegInfo{g[j], off, cnt, ldexpf(half_bits_to_float(xr[j]), s)};
+        atomicMin(wfirst + wave_of<WAVES>(off, wscale), static_cast<int>(idx));
+        ++idx;
+        off += cnt;
+      }
+    }
+    scale = s;
   }
-  // Fixed-point scale: a row of this slice sums at most n_seg terms, each at
-  // most max|w| * max|x| in magnitude; 2^s puts that bound at or below 2^30.
-  int s = 0;
-  const float bound = static_cast<float>(n_seg) * p.max_abs * __uint_as_float(xmax_bits);
-  if (bound > 0.f) {
-    int e;
-    frexpf(bound, &e);                 // bound < 2^e
-    s = min(max(30 - e, -64), 64);
-  }
-  __syncthreads();
-  for (int i = tid; i < static_cast<int>(n_seg); i += NT) seg[i].xs = ldexpf(seg[i].xs, s);
-
-  // ---- cut the flat group sequence into one range per wavefront -----------
-  // segment i goes to wavefront ~floor(off_i * WAVES / n_grp); wfirst[w] is the
-  // first segment of wavefront w, wfirst[WAVES] = n_seg.
-  // (any non-decreasing map of offsets to [0, WAVES) is valid; rounding in the
-  // float product keeps it non-decreasing)
-  const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
-  for (int i = tid; i < static_cast<int>(n_seg); i += NT) {
-    const int wi = min(static_cast<int>(static_cast<float>(seg[i].off) * wscale), WAVES - 1);
-    const int wp = i == 0 ? -1 : min(static_cast<int>(static_cast<float>(seg[i - 1].off) * wscale), WAVES - 1);
-    for (int w = wp + 1; w <= wi; ++w) wfirst[w] = i;
-    if (i == static_cast<int>(n_seg) - 1)
-      for (int w = wi + 1; w <= WAVES; ++w) wfirst[w] = static_cast<int>(n_seg);
-  }
-  if (n_seg == 0 && tid <= WAVES) wfirst[tid] = 0;
   __syncthreads();
 
   // ---- per-wavefront walk over passes of 64*G groups -----------------------
@@ -409,7 +470,16 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   // register copies force an early wait.  Passes past the end are idle (every
   // lane inactive, loads of group 0) and accumulate nothing.
   constexpr uint32_t P = kWave * G;
-  const int i_begin = wfirst[wv], i_end = wfirst[wv + 1];
+  // wavefront wv walks the segments [i_begin, i_end): the first segment of
+  // any wavefront at or after wv (n_seg if none), up to that of wv + 1
+  // (lane l < WAVES reads wfirst[l]; a suffix minimum over the row)
+  int i_begin, i_end;
+  {
+    const int f = row_suffix_min(lane < WAVES ? wfirst[lane] : INT_MAX);
+    const int wvu = __builtin_amdgcn_readfirstlane(wv);
+    i_begin = min(static_cast<int>(n_seg), __builtin_amdgcn_readlane(f, wvu));
+    i_end = min(static_cast<int>(n_seg), __builtin_amdgcn_readlane(f, wvu + 1));
+  }
   if (i_begin < i_end) {
     const Streams st = make_streams(p.values, p.runs, p.n_groups);
     int* scr = scr_all + wv * kWave * G;
@@ -446,7 +516,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   // ---- merge --------------------------------------------------------------
   if (p.KC == 1) {
     for (int r = tid; r < rows; r += NT)
-      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -s));
+      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -scale));
     return;
   }
   // Every slice adds one ticket per row with a returning 64-bit atomic: its
@@ -458,7 +528,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   // KC <= 63 keeps the biased sum below 2^56.
   constexpr long long kBias = 1ll << 49;
   constexpr unsigned long long kCount = 1ull << 56;
-  const int shift = p.s_glob - s;
+  const int shift = p.s_glob - scale;
   for (int r = tid; r < rows; r += NT) {
     const long long q = tile[r];
     long long v;
@@ -553,6 +623,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   }
   if (Kc < 1 || Kc > 4096) return CELTY_EINVAL;
   if (Kc > W->K) Kc = W->K;
+  if (Kc > kMaxCols * kWave * pl.waves) return CELTY_EINVAL;
   pl.Kc = Kc;
   pl.KC = (W->K + Kc - 1) / Kc;
   if (pl.KC > kMaxSlices) return CELTY_EINVAL;

@@ -164,6 +164,16 @@ def test_spmspv_plan_is_host_only():
     wide = _desc(K=200000)                                           # auto shape keeps <= 63 slices
     assert celty._plan(ctypes.byref(wide), None, ctypes.byref(out), ctypes.byref(nb), None) == CELTY_OK
     assert -(-200000 // out.cols_per_block) <= 63
+    assert out.cols_per_block <= 512 * out.waves_per_block
+    # at most 8 columns per lane in the selection: cols_per_block <= 512 * waves
+    for cols, waves, want in [(1024, 2, CELTY_OK), (1025, 2, CELTY_EINVAL), (2048, 4, CELTY_OK),
+                              (2049, 4, CELTY_EINVAL), (4096, 8, CELTY_OK), (4096, 4, CELTY_EINVAL)]:
+        L = celty_launch(cols, waves)
+        assert celty._plan(ctypes.byref(d), ctypes.byref(L), ctypes.byref(out), None, None) == want, (cols, waves)
+    narrow = _desc(K=1000)                                           # columns beyond K are not counted
+    L = celty_launch(4096, 2)
+    assert celty._plan(ctypes.byref(narrow), ctypes.byref(L), ctypes.byref(out), None, None) == CELTY_OK
+    assert out.cols_per_block == 1000
 
 
 @host_only

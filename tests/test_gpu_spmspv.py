@@ -108,9 +108,10 @@ def test_spmspv_fuzz(celty, torch_dev, M, K, R, ws, as_, groups):
     _check(y, p.W, p.mask, p.x, p.tau)
 
 
+# cols / (64 * waves) covers 1 to 8 columns per lane in the selection
 @pytest.mark.parametrize("launch", [(40, 2, 1), (41, 4, 2), (64, 2, 4), (64, 4, 1), (128, 8, 2), (256, 16, 4),
-                                    (1000, 4, 1), (1000, 4, 4), (4096, 4, 2), (4096, 16, 1), (700, 8, 4),
-                                    (2500, 2, 4)])
+                                    (1000, 4, 1), (1000, 4, 4), (2048, 4, 2), (4096, 16, 1), (700, 8, 4),
+                                    (1024, 2, 4), (129, 2, 1), (4096, 8, 1)])
 def test_launch_shapes_agree(celty, torch_dev, launch):
     _note(f"launch shape {launch}")
     p = workloads.random_small(77, 3000, 2500, ws=60, as_=50)
