@@ -296,61 +296,94 @@ __device__ __forceinline__ int next_pass_segment(const Pass<G>& a, uint32_t pb, 
   return min(a.end63 > pb + kWave * G ? a.sid63 : a.sid63 + 1, i_end - 1);
 }
 
-// Decodes one pass and adds its products into the fixed-point tile.  Returns
-// the segment-relative sum of (run + 1) through lane 63's last group (the
+// a + byte Q of b in one VALU operation (SDWA source select).
+template <int Q>
+__device__ __forceinline__ uint32_t add_byte(uint32_t a, uint32_t b) {
+  uint32_t r;
+  if constexpr (Q == 0)
+    asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+        : "=v"(r) : "v"(a), "v"(b));
+  else if constexpr (Q == 1)
+    asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+        : "=v"(r) : "v"(a), "v"(b));
+  else if constexpr (Q == 2)
+    asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+        : "=v"(r) : "v"(a), "v"(b));
+  else
+    asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+        : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Adds entry j's product at LDS byte address a + 4 * (j + 1), the constant in
+// the instruction's offset field.  (LDS operations complete in order, so the
+// compiler's waits for its own LDS accesses stay correct around this one; the
+// clobber keeps it in order with them.)
+template <int J>
+__device__ __forceinline__ void tile_add(uint32_t a, int v) {
+  asm volatile("ds_add_u32 %0, %1 offset:%2" : : "v"(a), "v"(v), "i"(4 * (J + 1)) : "memory");
+}
+
+// Decodes one pass and adds its products into the fixed-point tile at LDS
+// byte address tile_lds.  Row arithmetic is done on byte offsets, 4 * row: a
+// group's runs r_0..r_7 put entry j at 4 * (base + sum_{i<=j} (r_i + 1)), so
+// one running address advances by the byte 4 * r_j per entry and the
+// constant 4 * (j + 1) is an immediate.  Returns the
+// segment-relative sum of 4 * (run + 1) through lane 63's last group (the
 // carry when that segment goes on into the next pass), wavefront-uniform.
 template <int G>
-__device__ __forceinline__ int accumulate_pass(int* tile, const Pass<G>& a, int carry, int base_cap, int* scr,
-                                               int lane) {
-  uint32_t E[G], O[G];
-  int S[G], C[G];
+__device__ __forceinline__ int accumulate_pass(const Pass<G>& a, int carry4, int base4_cap, uint32_t tile_lds,
+                                               int* scr, int lane) {
+  uint32_t R4e[G], R4o[G];
+  int S4[G], C4[G];
   int T = 0;
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    // byte k of O: inclusive prefix of (run + 1) through entry 2k+1; byte k
-    // of E: the same through entry 2k.  The byte-wise running sum is two
-    // shift-adds (kept as such rather than the quarter-rate multiply by
-    // 0x01010101).
     const bool lv = (a.live >> i) & 1u;
     const uint32_t rw = lv ? a.rw[i] : 0u;
-    const uint32_t r_even = rw & 0x0F0F0F0Fu;
-    const uint32_t r_odd = (rw >> 4) & 0x0F0F0F0Fu;
-    const uint32_t pair = r_even + r_odd + 0x02020202u;
-    uint32_t half, o;
-    asm("v_lshl_add_u32 %0, %1, 8, %1" : "=v"(half) : "v"(pair));
-    asm("v_lshl_add_u32 %0, %1, 16, %1" : "=v"(o) : "v"(half));
-    O[i] = o;
-    E[i] = o - r_odd - 0x01010101u;
-    S[i] = lv ? static_cast<int>(o >> 24) : 0;   // the group's total
-    C[i] = T;                                     // before the group, within the lane
-    T += S[i];
+    R4e[i] = (rw << 2) & 0x3C3C3C3Cu;   // byte k: 4 * r_{2k}
+    R4o[i] = (rw >> 2) & 0x3C3C3C3Cu;   // byte k: 4 * r_{2k+1}
+    // 4 * sum of (run + 1) over the group
+    S4[i] = lv ? static_cast<int>(__builtin_amdgcn_sad_u8(R4e[i] + R4o[i], 0u, 32u)) : 0;
+    C4[i] = T;   // before the group, within the lane
+    T += S4[i];
   }
   const int incl = wave_inclusive_scan(T);
   const int X = incl - T;   // before the lane's first group, within the pass
-  // prefix sum before every flat position of the pass, for the segment heads
+  // prefix before every flat position of the pass, for the segment heads
 #pragma unroll
-  for (int i = 0; i < G; ++i) scr[G * lane + i] = X + C[i];
+  for (int i = 0; i < G; ++i) scr[G * lane + i] = X + C4[i];
   wave_lds_sync();
   int tail = 0;
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    const int Y = X + C[i];
+    const int Y = X + C4[i];
     const int at_head = scr[max(a.hpos[i], 0)];
-    const int rel = a.hpos[i] >= 0 ? Y - at_head : Y + carry;   // segment-relative
-    // row of entry j = base + prefix_j; base >= -1 and prefix_j <= 128, and the
-    // cap keeps even a corrupt stream inside the tile's slack
-    const int base = min(rel - 1, base_cap);
+    const int rel4 = a.hpos[i] >= 0 ? Y - at_head : Y + carry4;   // segment-relative
+    // entry j lands at base4 + sum_{i<=j} 4 r_i + 4 (j + 1) with base4 >= -4;
+    // the cap keeps even a corrupt stream inside the tile's slack
+    const uint32_t base4 = static_cast<uint32_t>(min(rel4 - 4, base4_cap)) + tile_lds;
     if ((a.live >> i) & 1u) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t w = q == 0 ? a.v[i].x : q == 1 ? a.v[i].y : q == 2 ? a.v[i].z : a.v[i].w;
-        const int re = base + static_cast<int>((E[i] >> (8 * q)) & 0xFFu);
-        const int ro = base + static_cast<int>((O[i] >> (8 * q)) & 0xFFu);
-        atomicAdd(tile + re, round_to_fixed(mul_lo_f16(w, a.xs[i])));
-        atomicAdd(tile + ro, round_to_fixed(mul_hi_f16(w, a.xs[i])));
-      }
+      const float xs = a.xs[i];
+      uint32_t ad = base4;
+      ad = add_byte<0>(ad, R4e[i]);
+      tile_add<0>(ad, round_to_fixed(mul_lo_f16(a.v[i].x, xs)));
+      ad = add_byte<0>(ad, R4o[i]);
+      tile_add<1>(ad, round_to_fixed(mul_hi_f16(a.v[i].x, xs)));
+      ad = add_byte<1>(ad, R4e[i]);
+      tile_add<2>(ad, round_to_fixed(mul_lo_f16(a.v[i].y, xs)));
+      ad = add_byte<1>(ad, R4o[i]);
+      tile_add<3>(ad, round_to_fixed(mul_hi_f16(a.v[i].y, xs)));
+      ad = add_byte<2>(ad, R4e[i]);
+      tile_add<4>(ad, round_to_fixed(mul_lo_f16(a.v[i].z, xs)));
+      ad = add_byte<2>(ad, R4o[i]);
+      tile_add<5>(ad, round_to_fixed(mul_hi_f16(a.v[i].z, xs)));
+      ad = add_byte<3>(ad, R4e[i]);
+      tile_add<6>(ad, round_to_fixed(mul_lo_f16(a.v[i].w, xs)));
+      ad = add_byte<3>(ad, R4o[i]);
+      tile_add<7>(ad, round_to_fixed(mul_hi_f16(a.v[i].w, xs)));
     }
-    if (i == G - 1) tail = rel + S[i];
+    if (i == G - 1) tail = rel4 + S4[i];
   }
   return __builtin_amdgcn_readlane(tail, kWave - 1);
 }
@@ -375,6 +408,9 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   constexpr int NT = WAVES * kWave;
   extern __shared__ __align__(16) unsigned char smem[];
   int* tile = reinterpret_cast<int*>(smem);
+  // the tile's LDS byte address (for the accumulation's own LDS instructions)
+  const uint32_t tile_lds = static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem));
   SegInfo* seg = reinterpret_cast<SegInfo*>(smem + p.seg_off);
   int* scr_all = reinterpret_cast<int*>(smem + p.scr_off);
   uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 3*WAVES
@@ -384,7 +420,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   const int t = blockIdx.x / p.KC, c = blockIdx.x - t * p.KC;
   const int row0 = t * p.R;
   const int rows = min(p.R, p.M - row0);
-  const int base_cap = p.R + 7;
+  const int base4_cap = 4 * (p.R + 7);   // tile byte address cap of a group base
 
   for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0;
   for (int i = tid; i < NT * G; i += NT) scr_all[i] = 0;
@@ -496,12 +532,12 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
       pf += P;
     }
     uint32_t pb = pb0;    // flat start of the pass being accumulated
-    int carry = 0;        // sum of (run + 1) over its first segment's earlier groups
+    int carry = 0;        // 4 * sum of (run + 1) over its first segment's earlier groups
     for (int done = 0; done < n_pass; done += DEPTH) {
 #pragma unroll
       for (int d = 0; d < DEPTH; ++d) {
         if (pb < pe) {   // wavefront-uniform
-          const int tail = accumulate_pass<G>(tile, ring[d], carry, base_cap, scr, lane);
+          const int tail = accumulate_pass<G>(ring[d], carry, base4_cap, tile_lds, scr, lane);
           carry = ring[d].end63 > pb + P ? tail : 0;
         }
         pb += P;
