@@ -35,8 +35,12 @@ PEAK_HBM_GBPS = 8000.0   # MI355X HBM3E, published
 METRIC = "µs/SpMSpV + effective HBM GB/s (% peak), 4096×4096 at 70% dual sparsity"
 COLD_BYTES = 1 << 30
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_01536_amd", "csrc", "spmspv.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+PROFILES = os.path.join(ROOT, "profiles")
 CALIBRATION_BYTES = 256 << 20
+
+
+def traffic_file(workload_key: str) -> str:
+    return os.path.join(PROFILES, f"spmspv_{workload_key}_traffic.json")
 
 
 def kernel_source_sha() -> str:
@@ -49,13 +53,56 @@ def measured_traffic(workload_key: str):
     """HBM bytes per launch from the committed counter profile, or None when
     the profile is missing, for another workload, or older than the kernel."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(workload_key)) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
     if rec.get("kernel_source_sha256") != kernel_source_sha() or rec.get("workload_key") != workload_key:
         return None
     return rec.get("traffic_bytes_per_launch")
+
+
+def _counter_per_dispatch(csv_path: str, name_parts) -> list:
+    """Per-dispatch sums of a rocprofv3 counter CSV for kernels whose name
+    contains any of name_parts."""
+    import csv
+    vals = {}
+    with open(csv_path) as f:
+        for row in csv.DictReader(f):
+            if any(n in row["Kernel_Name"] for n in name_parts):
+                vals[row["Dispatch_Id"]] = vals.get(row["Dispatch_Id"], 0.0) + float(row["Counter_Value"])
+    return list(vals.values())
+
+
+def record_traffic(workload_key: str, paths, commands) -> int:
+    """Turns four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE of this
+    benchmark, then of the plain copy) into HBM bytes per launch: each
+    counter's median per SpMSpV dispatch, scaled by the bytes the copy moved
+    over what the same counter read for it.  Writes the record that
+    measured_traffic() reads."""
+    import statistics
+    fetch, write, cfetch, cwrite = paths
+    k_f = _counter_per_dispatch(fetch, ["spmspv_kernel"])
+    k_w = _counter_per_dispatch(write, ["spmspv_kernel"])
+    c_f = _counter_per_dispatch(cfetch, ["elementwise_kernel", "copy"])
+    c_w = _counter_per_dispatch(cwrite, ["elementwise_kernel", "copy"])
+    if not (k_f and k_w and c_f and c_w):
+        print("record-traffic: a counter file has no matching dispatches", file=sys.stderr)
+        return 1
+    fk, wk = statistics.median(k_f), statistics.median(k_w)
+    cf, cw = statistics.median(c_f), statistics.median(c_w)
+    ff, wf = CALIBRATION_BYTES / (cf * 1024.0), CALIBRATION_BYTES / (cw * 1024.0)
+    rec = {"workload_key": workload_key, "kernel_source_sha256": kernel_source_sha(),
+           "fetch_kib_per_dispatch": fk, "write_kib_per_dispatch": wk, "dispatches": [len(k_f), len(k_w)],
+           "copy_fetch_kib": cf, "copy_write_kib": cw, "copy_bytes": CALIBRATION_BYTES,
+           "fetch_factor": ff, "write_factor": wf,
+           "traffic_bytes_per_launch": int(round(fk * 1024.0 * ff + wk * 1024.0 * wf)),
+           "commands": commands}
+    with open(traffic_file(workload_key), "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec))
+    return 0
 
 
 def copy_calibration() -> int:
@@ -179,6 +226,8 @@ def main() -> int:
     ap.add_argument("--hot", action="store_true", help="reuse one copy (cache-resident; diagnostic)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of a known size (counter calibration)")
+    ap.add_argument("--record-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="host only: write this workload's HBM traffic record from rocprofv3 counter CSVs")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration()
@@ -194,12 +243,24 @@ def main() -> int:
     import paper_2608_01536_amd as celty
     import workloads
 
-    dev = torch.device("cuda:0")
     M, K = args.M, args.K
     headline = (M, K, args.ws, args.as_) == (4096, 4096, 70.0, 70.0)
     p = workloads.make_problem(2, M, K, args.ws, args.as_, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
     R = args.R or celty.default_tile_rows(M, K)
     enc = celty.celty_encode(p.W, p.mask, R)
+    launch = (args.cols, args.waves) if (args.cols or args.waves) else None
+    plan = celty.celty_spmspv_plan(enc, launch)
+    workload_key = (f"{M}x{K}-ws{args.ws:g}-as{args.as_:g}-R{R}-"
+                    f"{plan['cols_per_block']}x{plan['waves_per_block']}x{plan['groups_per_lane']}")
+    if args.record_traffic:
+        flags = f" --M {M} --K {K} --ws {args.ws:g} --as {args.as_:g}" + (f" --R {args.R}" if args.R else "") + \
+                (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "")
+        cmds = [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py "
+                f"--steps 200 --warmup 20 --no-cpu --no-dense{flags}" for c in ("FETCH_SIZE", "WRITE_SIZE")]
+        cmds += [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py --copy-calibration"
+                 for c in ("FETCH_SIZE", "WRITE_SIZE")]
+        return record_traffic(workload_key, args.record_traffic, cmds)
+    dev = torch.device("cuda:0")
     b_alg, e_a, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
     sbytes = stored_bytes(enc)
     ncopies = 1 if args.hot else max(2, -(-COLD_BYTES // sbytes))
@@ -208,8 +269,6 @@ def main() -> int:
     x = torch.from_numpy(p.x.view(np.int16)).to(dev)
     y = torch.empty(M, dtype=torch.int16, device=dev)
     ws = celty.new_workspace(base, dev)
-    launch = (args.cols, args.waves) if (args.cols or args.waves) else None
-    plan = celty.celty_spmspv_plan(base, launch)
     def step(i):
         # stream = None: the binding launches on torch's current stream, which
         # is the capture stream while a graph is being recorded
@@ -258,7 +317,6 @@ def main() -> int:
 
     gbps_step = b_alg / us_step / 1e3
     achieved = b_alg / us_kernel / 1e3
-    workload_key = f"{M}x{K}-ws{args.ws:g}-as{args.as_:g}-R{R}-{plan['cols_per_block']}x{plan['waves_per_block']}"
     traffic = None if args.hot else measured_traffic(workload_key)
     workload = (f"{M}x{K} fp16 W (out x in), {args.ws:g}% unstructured weight sparsity + "
                 f"{args.as_:g}% activation sparsity (Laplace x, magnitude threshold), batch 1")

@@ -139,15 +139,24 @@ celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* ma
 celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int32_t* count,
                           void* stream);
 
-/* Launch shape of celty_spmspv_ex.  Zero fields mean "choose automatically".
- * The K columns are cut into ceil(K / cols_per_block) slices, at most 63
- * (the merge counts slices in one byte of a 64-bit word).  A workgroup's
- * lanes scan at most 8 columns each: cols_per_block <= 512 * waves_per_block. */
+/* Launch shape of celty_spmspv_ex.  Zero fields mean "choose automatically":
+ * 16 wavefronts per workgroup for R >= 1024, else 8; slices sized for about
+ * 4096 / waves_per_block workgroups (16 wavefronts on each of 256 compute
+ * units); one group per lane.  The K columns are cut into
+ * ceil(K / cols_per_block) slices, at most 63 (the merge counts slices in one
+ * byte of a 64-bit word).  A workgroup's lanes scan at most 8 columns each:
+ * cols_per_block <= 512 * waves_per_block. */
 typedef struct celty_launch {
   int32_t cols_per_block;   /* columns of x one workgroup scans (1..4096) */
   int32_t waves_per_block;  /* 2, 4, 8 or 16 wavefronts of 64 lanes */
   int32_t groups_per_lane;  /* 1, 2 or 4 eight-entry groups per lane per pass */
 } celty_launch;
+
+/* A tile height R for encoding an M x K matrix for celty_spmspv (host only):
+ * the largest power of two at or below M / 8, clamped to [256, 2048], which
+ * gives 8 to 16 row tiles for the LLM projection shapes and keeps one tile's
+ * accumulator (4 * (R + 136) bytes of LDS) small.  0 when M < 1. */
+int32_t celty_default_tile_rows(int32_t M, int32_t K);
 
 /* Bytes of device workspace celty_spmspv needs for this shape: one 64-bit
  * merge slot per output row, rounded up to 256 bytes. */

@@ -77,6 +77,7 @@ _ws_init = _sig("celty_spmspv_workspace_init", ctypes.c_int, _p, _sz, _p)
 _spmspv = _sig("celty_spmspv", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz, _p)
 _spmspv_ex = _sig("celty_spmspv_ex", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz,
                   ctypes.POINTER(celty_launch), _p)
+_default_tile_rows = _sig("celty_default_tile_rows", _i32, _i32, _i32)
 _plan = _sig("celty_spmspv_plan", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), ctypes.POINTER(celty_launch),
              ctypes.POINTER(celty_launch), ctypes.POINTER(_i64), ctypes.POINTER(_i64))
 _status_string = _sig("celty_status_string", ctypes.c_char_p, ctypes.c_int)
@@ -288,16 +289,8 @@ def celty_spmspv_plan(W, launch=None) -> dict:
 
 
 def default_tile_rows(M: int, K: int) -> int:
-    """Tile height R used for the benchmark encodings (rows per LDS tile).
-
-    Small matrices need short tiles for enough row-tile parallelism on 256
-    CUs; tall ones take longer tiles, which spend fewer bytes on group
-    pointers and on the 8-entry alignment of each segment."""
-    if M <= 4096:
-        return 128
-    if M <= 16384:
-        return 256
-    return 512
+    """Tile height R for encoding an M x K matrix (celty_default_tile_rows)."""
+    return int(_default_tile_rows(int(M), int(K)))
 
 
 __all__ = [

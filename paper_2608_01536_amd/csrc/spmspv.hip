@@ -30,6 +30,7 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstdint>
@@ -647,14 +648,18 @@ celty_status check_header(const celty_rlc_csc* W) {
 celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl) {
   if (celty_status st = check_header(W)) return st;
   pl.T = W->T;
-  pl.waves = (cfg && cfg->waves_per_block) ? cfg->waves_per_block : 8;
+  // automatic shape: 16 wavefronts per compute unit on 256 compute units,
+  // as one workgroup of 16 (tiles of 1024 rows or more) or two of 8
+  pl.waves = (cfg && cfg->waves_per_block) ? cfg->waves_per_block : (W->R >= 1024 ? 16 : 8);
   if (pl.waves != 2 && pl.waves != 4 && pl.waves != 8 && pl.waves != 16) return CELTY_EINVAL;
   int Kc = cfg ? cfg->cols_per_block : 0;
   if (Kc == 0) {
-    // slices of 512 columns (fewer than 64 slices: the merge's count byte)
-    int64_t kc = 512;
-    const int64_t min_kc = (W->K + kMaxSlices - 1) / kMaxSlices;
-    if (kc < min_kc) kc = (min_kc + 63) / 64 * 64;
+    // about 4096 / waves workgroups: T row tiles times KC slices (at most
+    // 63, the merge's count byte) of a multiple of 64 columns
+    const int64_t target = 4096 / pl.waves;
+    const int64_t kcs = std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, (target + W->T / 2) / W->T));
+    int64_t kc = ((W->K + kcs - 1) / kcs + 63) / 64 * 64;
+    kc = std::min<int64_t>(kc, std::min(4096, kMaxCols * kWave * pl.waves));
     Kc = static_cast<int>(kc);
   }
   if (Kc < 1 || Kc > 4096) return CELTY_EINVAL;
@@ -663,15 +668,10 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   pl.Kc = Kc;
   pl.KC = (W->K + Kc - 1) / Kc;
   if (pl.KC > kMaxSlices) return CELTY_EINVAL;
-  pl.groups = cfg ? cfg->groups_per_lane : 0;
-  if (pl.groups == 0) {
-    // groups per lane per pass: enough passes per wavefront to keep them
-    // busy, as few as possible to amortise the per-pass bookkeeping
-    // (entries per wavefront estimated at half the columns active)
-    const double density = static_cast<double>(W->n_entries) / (static_cast<double>(W->M) * W->K);
-    const double per_wave = 0.5 * Kc * static_cast<double>(W->R) * density / pl.waves;
-    pl.groups = per_wave >= 4 * 2048.0 ? 4 : per_wave >= 4 * 1024.0 ? 2 : 1;
-  }
+  // one group per lane per pass unless asked otherwise: with several, the
+  // lanes of one LDS add instruction land G groups apart, which costs more
+  // bank conflicts than the bookkeeping it saves
+  pl.groups = (cfg && cfg->groups_per_lane) ? cfg->groups_per_lane : 1;
   if (pl.groups != 1 && pl.groups != 2 && pl.groups != 4) return CELTY_EINVAL;
   // the tile (int32) goes first: R rows, then 7 alignment rows and 128 rows
   // of slack that bound where a corrupt stream could write (base is capped at
@@ -716,6 +716,14 @@ celty_status launch(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+extern "C" int32_t celty_default_tile_rows(int32_t M, int32_t K) {
+  (void)K;
+  if (M < 1) return 0;
+  int32_t r = 256;
+  while (r < 2048 && 2 * r <= M / 8) r *= 2;
+  return r;
+}
 
 extern "C" size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R) {
   (void)K;

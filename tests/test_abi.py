@@ -32,7 +32,7 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for want in ("celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv",
                  "celty_spmspv_ex", "celty_spmspv_plan", "celty_spmspv_workspace_bytes",
-                 "celty_spmspv_workspace_init", "celty_status_string"):
+                 "celty_spmspv_workspace_init", "celty_status_string", "celty_default_tile_rows"):
         assert want in names
 
 
@@ -49,6 +49,14 @@ def test_status_strings():
     for st in range(6):
         assert celty.celty_status_string(st).startswith("CELTY_")
     assert "unknown" in celty.celty_status_string(99)
+
+
+def test_default_tile_rows():
+    # largest power of two <= M / 8, clamped to [256, 2048]
+    for M, want in [(1, 256), (1024, 256), (4096, 512), (4095, 256), (5120, 512), (8192, 1024), (11008, 1024),
+                    (13824, 1024), (16384, 2048), (28672, 2048), (1 << 20, 2048)]:
+        assert celty.default_tile_rows(M, 4096) == want, M
+    assert celty._default_tile_rows(0, 5) == 0
 
 
 def test_workspace_bytes():
