@@ -105,6 +105,108 @@ def record_traffic(workload_key: str, paths, commands) -> int:
     return 0
 
 
+def sequence_bench(args) -> int:
+    """One decode step of config 3, 4 or 5: the 7 projections of every layer,
+    timed as one HIP graph per schedule.  Layers are distinct device copies of
+    layer 0's encodings (same values, separate memory), so every step streams
+    all of its weights from HBM; at least 1 GiB of copies is rotated when the
+    step itself is smaller."""
+    import torch
+    import torch.nn.functional as F
+
+    import paper_2608_01536_amd as celty
+    import workloads
+
+    cfg = args.sequence
+    c = workloads.CONFIGS[cfg]
+    as_ = args.seq_as if args.seq_as is not None else (c["as_"] if not isinstance(c["as_"], tuple) else 60)
+    n_layers = args.layers or c["n_layers"]
+    dev = torch.device("cuda:0")
+    probs = workloads.layer_problems(cfg, 0, 0, as_)
+    names = [p.meta["proj_name"] for p in probs]
+    Rs = [celty.default_tile_rows(*p.W.shape) for p in probs]
+    encs = [celty.celty_encode(p.W, p.mask, R) for p, R in zip(probs, Rs)]
+    alg = [algorithmic_bytes_from_encoding(e, p.x, p.tau)[0] for e, p in zip(encs, probs)]
+    layer_bytes = sum(stored_bytes(e) for e in encs)
+    n_copies = max(n_layers, -(-COLD_BYTES // layer_bytes))
+    print(f"[sequence] config {cfg}: {n_layers} layers, as{as_:g}, {n_copies} device copies of "
+          f"{layer_bytes / 1e6:.1f} MB", file=sys.stderr, flush=True)
+    base = [e.to_device(dev) for e in encs]
+    del encs
+    layers = [base] + [[W.clone_to() for W in base] for _ in range(n_copies - 1)]
+    xg = {}
+    for p, pr in zip(probs, c["layers"]):
+        if pr.x_group not in xg:
+            xg[pr.x_group] = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    xs = [xg[pr.x_group] for pr in c["layers"]]
+    taus = [p.tau for p in probs]
+    ys = [torch.empty(p.W.shape[0], dtype=torch.int16, device=dev) for p in probs]
+    wss = [celty.new_workspace(W, dev) for W in base]
+    # batched schedule: consecutive projections reading the same x share a launch
+    groups, prev = [], None
+    for i, pr in enumerate(c["layers"]):
+        if pr.x_group == prev:
+            groups[-1].append(i)
+        else:
+            groups.append([i])
+        prev = pr.x_group
+    bws = [celty.new_batch_workspace([base[i] for i in g], dev) for g in groups]
+    steps = max(2, -(-n_copies // n_layers)) * 2
+
+    def step_sequential(s):
+        for l in range(n_layers):
+            L = layers[(s * n_layers + l) % n_copies]
+            for i in range(len(L)):
+                celty.celty_spmspv(L[i], xs[i], taus[i], ys[i], wss[i])
+
+    def step_batched(s):
+        for l in range(n_layers):
+            L = layers[(s * n_layers + l) % n_copies]
+            for g, w in zip(groups, bws):
+                celty.celty_spmspv_batch([L[i] for i in g], [xs[i] for i in g], [taus[i] for i in g],
+                                         [ys[i] for i in g], w)
+
+    out = {"sequence": cfg, "name": c["name"], "activation_sparsity_pct": as_, "layers": n_layers,
+           "device_copies": n_copies, "data": "synthetic",
+           "alg_bytes_per_step": int(n_layers * sum(alg)), "stored_bytes_per_layer": int(layer_bytes)}
+    for label, fn, launches in (("sequential", step_sequential, len(names)), ("batched", step_batched, len(groups))):
+        for i in range(2):
+            fn(i)
+        torch.cuda.synchronize()
+        us, samples = time_graph(torch, fn, steps, replays=3)
+        out[label] = {"us_per_step": round(us, 2), "launches_per_step": n_layers * launches,
+                      "GBps": round(out["alg_bytes_per_step"] / us / 1e3, 1),
+                      "pct_peak_hbm": round(100 * out["alg_bytes_per_step"] / us / 1e3 / PEAK_HBM_GBPS, 2)}
+        print(f"[sequence] {label}: {us:.1f} us/step", file=sys.stderr, flush=True)
+    per = {}
+    for i, nm in enumerate(names):
+        fn = lambda j, i=i: celty.celty_spmspv(layers[j % n_copies][i], xs[i], taus[i], ys[i], wss[i])
+        us, _ = time_graph(torch, fn, max(n_copies, 100), replays=3)
+        per[nm] = {"us": round(us, 3), "M": probs[i].W.shape[0], "K": probs[i].W.shape[1], "R": Rs[i],
+                   "GBps": round(alg[i] / us / 1e3, 1)}
+    out["per_projection"] = per
+    if not args.no_dense:
+        dense = {}
+        for i, nm in enumerate(names):
+            M, K = probs[i].W.shape
+            if (M, K) not in dense:
+                Wf = torch.from_numpy(np.where(probs[i].mask != 0, probs[i].W, np.float16(0))).to(dev)
+                nd = max(2, -(-COLD_BYTES // (2 * M * K)))
+                dc = [Wf] + [Wf.clone() for _ in range(nd - 1)]
+                xd = torch.zeros(1, K, dtype=torch.float16, device=dev)
+                for j in range(5):
+                    F.linear(xd, dc[j % nd])
+                dense[(M, K)], _ = time_graph(torch, lambda j: F.linear(xd, dc[j % nd]), max(nd, 100), replays=3)
+                del dc, Wf
+                torch.cuda.empty_cache()
+        d_step = n_layers * sum(dense[p.W.shape] for p in probs)
+        out["dense_gemv_us_per_step"] = round(d_step, 2)
+        out["dense_note"] = "sum over the layer's shapes of F.linear fp16 batch-1 times (cold copies) x layers"
+        out["speedup_vs_dense"] = {k: round(d_step / out[k]["us_per_step"], 3) for k in ("sequential", "batched")}
+    print(json.dumps(out))
+    return 0
+
+
 def copy_calibration() -> int:
     """A plain device copy of CALIBRATION_BYTES (reads and writes that many
     bytes once): run under the FETCH_SIZE / WRITE_SIZE counters to scale them."""
@@ -228,6 +330,10 @@ def main() -> int:
                     help="only run a plain copy of a known size (counter calibration)")
     ap.add_argument("--record-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="host only: write this workload's HBM traffic record from rocprofv3 counter CSVs")
+    ap.add_argument("--sequence", type=int, choices=(3, 4, 5),
+                    help="time one decode step of config 3, 4 or 5 (its own JSON line)")
+    ap.add_argument("--layers", type=int, default=0, help="layers of --sequence (0 = the config's)")
+    ap.add_argument("--seq-as", type=float, default=None, help="activation sparsity of --sequence")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration()
@@ -236,6 +342,9 @@ def main() -> int:
         print("bench.py runs on one GPU only: the SpMSpV path here is single-GPU "
               "(row-sharding across GPUs is a design note, not built); use --gpus 1", file=sys.stderr)
         return 2
+
+    if args.sequence:
+        return sequence_bench(args)
 
     import torch
     import torch.nn.functional as F

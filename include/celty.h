@@ -202,6 +202,35 @@ celty_status celty_spmspv_ex(const celty_rlc_csc* W, const void* x, float tau, v
                              void* workspace, size_t workspace_bytes,
                              const celty_launch* launch, void* stream);
 
+/*
+ * Several independent SpMSpVs in one launch (Section 3.1's product for each;
+ * one launch instead of n: projections of a decoder layer that read the same
+ * activation, q/k/v or gate/up, pass the same x).
+ *   n          1..8 products.
+ *   W[i]       descriptor with device pointers, as for celty_spmspv; the
+ *              products may have different shapes and tile heights.
+ *   x[i], tau[i], y[i]
+ *              as for celty_spmspv; x pointers may repeat, a y may not
+ *              overlap any x, any other y or the workspace.
+ *   workspace  device buffer of at least
+ *              celty_spmspv_batch_workspace_bytes(n, W) bytes (product i's
+ *              slots follow those of products 0..i-1), zero-filled before
+ *              first use and left zero-filled by every completed call.
+ *   launch     as for celty_spmspv_ex; cols_per_block applies to every product,
+ *              the automatic choice is made per product, with 16 wavefronts
+ *              when any product has R >= 1024.
+ * Results are those of n separate celty_spmspv_ex calls with the same launch.
+ * Errors: EINVAL (n outside 1..8, null arrays, any product's celty_spmspv
+ *         error, overlapping buffers, short workspace), EHIP.
+ */
+celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const* W, const void* const* x,
+                                const float* tau, void* const* y, void* workspace,
+                                size_t workspace_bytes, const celty_launch* launch, void* stream);
+
+/* Workspace bytes of celty_spmspv_batch: the sum over the products of
+ * celty_spmspv_workspace_bytes (host only; 0 for n outside 1..8 or null). */
+size_t celty_spmspv_batch_workspace_bytes(int32_t n, const celty_rlc_csc* const* W);
+
 /* The launch shape celty_spmspv_ex would use for W and `launch` (host only):
  * fills *resolved and, if not NULL, the workgroup count and LDS bytes. */
 celty_status celty_spmspv_plan(const celty_rlc_csc* W, const celty_launch* launch,

@@ -78,6 +78,10 @@ _spmspv = _sig("celty_spmspv", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, 
 _spmspv_ex = _sig("celty_spmspv_ex", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz,
                   ctypes.POINTER(celty_launch), _p)
 _default_tile_rows = _sig("celty_default_tile_rows", _i32, _i32, _i32)
+_desc_pp = ctypes.POINTER(ctypes.POINTER(celty_rlc_csc))
+_batch = _sig("celty_spmspv_batch", ctypes.c_int, _i32, _desc_pp, ctypes.POINTER(_p), ctypes.POINTER(_f32),
+              ctypes.POINTER(_p), _p, _sz, ctypes.POINTER(celty_launch), _p)
+_batch_ws_bytes = _sig("celty_spmspv_batch_workspace_bytes", _sz, _i32, _desc_pp)
 _plan = _sig("celty_spmspv_plan", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), ctypes.POINTER(celty_launch),
              ctypes.POINTER(celty_launch), ctypes.POINTER(_i64), ctypes.POINTER(_i64))
 _status_string = _sig("celty_status_string", ctypes.c_char_p, ctypes.c_int)
@@ -278,6 +282,38 @@ def celty_spmspv_ex(W: DeviceRlcCsc, x, tau: float, y, workspace, launch=None, s
                       None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_ex")
 
 
+def _desc_array(Ws):
+    descs = [W.desc() for W in Ws]
+    arr = (ctypes.POINTER(celty_rlc_csc) * len(descs))(*[ctypes.pointer(d) for d in descs])
+    return descs, arr
+
+
+def celty_spmspv_batch_workspace_bytes(Ws) -> int:
+    descs, arr = _desc_array(Ws)
+    return int(_batch_ws_bytes(len(descs), arr))
+
+
+def new_batch_workspace(Ws, device=None):
+    """A zero-filled device workspace for celty_spmspv_batch over Ws."""
+    torch = _torch()
+    n = celty_spmspv_batch_workspace_bytes(Ws)
+    return torch.zeros(n, dtype=torch.uint8, device=device if device is not None else Ws[0].gptr.device)
+
+
+def celty_spmspv_batch(Ws, xs, taus, ys, workspace, launch=None, stream=None) -> None:
+    """n products y_i = W_i x_i (threshold tau_i) in one launch."""
+    n = len(Ws)
+    if not (len(xs) == len(taus) == len(ys) == n):
+        raise ValueError("Ws, xs, taus and ys must have the same length")
+    descs, arr = _desc_array(Ws)
+    xp = (_p * n)(*[_dev_ptr(x, 2, "x") for x in xs])
+    yp = (_p * n)(*[_dev_ptr(y, 2, "y") for y in ys])
+    tp = (_f32 * n)(*[float(t) for t in taus])
+    ls = _launch_struct(launch)
+    _check(_batch(n, arr, xp, tp, yp, _dev_ptr(workspace, 1, "workspace"), workspace.numel(),
+                  None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_batch")
+
+
 def celty_spmspv_plan(W, launch=None) -> dict:
     d = W.desc()
     ls = _launch_struct(launch)
@@ -296,6 +332,7 @@ def default_tile_rows(M: int, K: int) -> int:
 __all__ = [
     "default_tile_rows",
     "celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv", "celty_spmspv_ex",
+    "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "new_batch_workspace",
     "celty_spmspv_plan", "celty_spmspv_workspace_bytes", "celty_spmspv_workspace_init", "celty_status_string",
     "new_workspace", "HostRlcCsc", "DeviceRlcCsc", "CeltyError", "celty_rlc_csc", "celty_launch",
 ]

@@ -404,9 +404,25 @@ struct KernelArgs {
   int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS (the tile is at 0)
 };
 
+// Up to kMaxBatch independent products in one launch: product i owns
+// workgroups [block_start[i], block_start[i + 1]).
+constexpr int kMaxBatch = 8;
+struct BatchArgs {
+  int n;
+  int block_start[kMaxBatch + 1];
+  KernelArgs prod[kMaxBatch];
+};
+
 template <int WAVES, int G, int DEPTH>
-__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
+__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(BatchArgs ba) {
   constexpr int NT = WAVES * kWave;
+  // this workgroup's product (workgroup-uniform) and its index within it
+  int pi = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxBatch; ++i)
+    pi = (i < ba.n && static_cast<int>(blockIdx.x) >= ba.block_start[i]) ? i : pi;
+  const KernelArgs& p = ba.prod[pi];
+  const int blk = static_cast<int>(blockIdx.x) - ba.block_start[pi];
   extern __shared__ __align__(16) unsigned char smem[];
   int* tile = reinterpret_cast<int*>(smem);
   // the tile's LDS byte address (for the accumulation's own LDS instructions)
@@ -418,7 +434,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
   int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const int t = blockIdx.x / p.KC, c = blockIdx.x - t * p.KC;
+  const int t = blk / p.KC, c = blk - t * p.KC;
   const int row0 = t * p.R;
   const int rows = min(p.R, p.M - row0);
   const int base4_cap = 4 * (p.R + 7);   // tile byte address cap of a group base
@@ -691,28 +707,87 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   return CELTY_OK;
 }
 
+// The launch: total workgroups and the largest LDS footprint of the batch.
+struct Launch {
+  int waves = 8, groups = 1;
+  int64_t blocks = 0;
+  size_t lds = 0;
+};
+
 template <int WAVES, int G, int DEPTH>
-celty_status launch_shape(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
+celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
   static bool attr_set = false;
-  if (pl.lds > 64 * 1024 && !attr_set) {
+  if (ln.lds > 64 * 1024 && !attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&spmspv_kernel<WAVES, G, DEPTH>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds) != hipSuccess)
       return CELTY_EHIP;
     attr_set = true;
   }
-  hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(pl.blocks)), dim3(WAVES * kWave),
-                     pl.lds, stream, a);
+  hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.blocks)), dim3(WAVES * kWave),
+                     ln.lds, stream, a);
   return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
 }
 
 template <int WAVES>
-celty_status launch(const Plan& pl, const KernelArgs& a, hipStream_t stream) {
-  switch (pl.groups) {
-    case 1: return launch_shape<WAVES, 1, 3>(pl, a, stream);
-    case 2: return launch_shape<WAVES, 2, 2>(pl, a, stream);
-    case 4: return launch_shape<WAVES, 4, 2>(pl, a, stream);
+celty_status launch_groups(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
+  switch (ln.groups) {
+    case 1: return launch_shape<WAVES, 1, 3>(ln, a, stream);
+    case 2: return launch_shape<WAVES, 2, 2>(ln, a, stream);
+    case 4: return launch_shape<WAVES, 4, 2>(ln, a, stream);
     default: return CELTY_EINVAL;
   }
+}
+
+celty_status launch(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
+  switch (ln.waves) {
+    case 2: return launch_groups<2>(ln, a, stream);
+    case 4: return launch_groups<4>(ln, a, stream);
+    case 8: return launch_groups<8>(ln, a, stream);
+    case 16: return launch_groups<16>(ln, a, stream);
+    default: return CELTY_EINVAL;
+  }
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+// Validates one product's pointers and fills its kernel arguments.
+celty_status product_args(const celty_rlc_csc* W, const Plan& pl, const void* x, float tau, void* y, void* ws,
+                          KernelArgs& a) {
+  if (!x || !y || misaligned(x, 2) || misaligned(y, 2) || std::isnan(tau)) return CELTY_EINVAL;
+  if (overlaps(x, 2u * static_cast<size_t>(W->K), y, 2u * static_cast<size_t>(W->M))) return CELTY_EINVAL;
+  a.gptr = W->gptr;
+  a.values = reinterpret_cast<const uint4*>(W->values);
+  a.runs = W->runs;
+  a.x = static_cast<const unsigned short*>(x);
+  a.y = static_cast<unsigned short*>(y);
+  a.ws = static_cast<unsigned long long*>(ws);
+  // merge scale: any row sum is at most K * max|w| * 65504 (the largest
+  // finite fp16 |x|); 2^s_glob maps that bound to at most 2^48
+  a.s_glob = 0;
+  {
+    const double bound = static_cast<double>(W->K) * static_cast<double>(W->max_abs) * 65504.0;
+    if (bound > 0.0) {
+      int e;
+      std::frexp(bound, &e);
+      a.s_glob = 48 - e;
+    }
+  }
+  a.tau = tau;
+  a.max_abs = W->max_abs;
+  a.n_groups = static_cast<uint32_t>(W->n_groups);
+  a.M = W->M;
+  a.K = W->K;
+  a.R = W->R;
+  a.Kc = pl.Kc;
+  a.KC = pl.KC;
+  a.tile_slots = pl.tile_slots;
+  a.seg_off = pl.seg_off;
+  a.scr_off = pl.scr_off;
+  a.misc_off = pl.misc_off;
+  return CELTY_OK;
 }
 
 }  // namespace
@@ -755,53 +830,67 @@ extern "C" celty_status celty_spmspv_plan(const celty_rlc_csc* W, const celty_la
 extern "C" celty_status celty_spmspv_ex(const celty_rlc_csc* W, const void* x, float tau, void* y,
                                         void* workspace, size_t workspace_bytes, const celty_launch* launch_cfg,
                                         void* stream) {
-  Plan pl;
-  if (celty_status st = make_plan(W, launch_cfg, pl)) return st;
-  if (!x || !y || misaligned(x, 2) || misaligned(y, 2) || std::isnan(tau)) return CELTY_EINVAL;
-  const uintptr_t xb = reinterpret_cast<uintptr_t>(x), yb = reinterpret_cast<uintptr_t>(y);
-  if (xb < yb + 2u * static_cast<uintptr_t>(W->M) && yb < xb + 2u * static_cast<uintptr_t>(W->K))
-    return CELTY_EINVAL;   // x and y overlap
-  const size_t need = celty_spmspv_workspace_bytes(W->M, W->K, W->R);
+  return celty_spmspv_batch(1, &W, &x, &tau, &y, workspace, workspace_bytes, launch_cfg, stream);
+}
+
+extern "C" size_t celty_spmspv_batch_workspace_bytes(int32_t n, const celty_rlc_csc* const* W) {
+  if (n < 1 || n > kMaxBatch || !W) return 0;
+  size_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    if (!W[i]) return 0;
+    total += celty_spmspv_workspace_bytes(W[i]->M, W[i]->K, W[i]->R);
+  }
+  return total;
+}
+
+extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const* W, const void* const* x,
+                                           const float* tau, void* const* y, void* workspace,
+                                           size_t workspace_bytes, const celty_launch* launch_cfg, void* stream) {
+  if (n < 1 || n > kMaxBatch || !W || !x || !tau || !y) return CELTY_EINVAL;
+  for (int i = 0; i < n; ++i)
+    if (celty_status st = check_header(W[i])) return st;
+  // one wavefront count and group count for the whole launch
+  Launch ln;
+  if (launch_cfg && launch_cfg->waves_per_block) {
+    ln.waves = launch_cfg->waves_per_block;
+  } else {
+    ln.waves = 8;
+    for (int i = 0; i < n; ++i)
+      if (W[i]->R >= 1024) ln.waves = 16;
+  }
+  ln.groups = (launch_cfg && launch_cfg->groups_per_lane) ? launch_cfg->groups_per_lane : 1;
+  const celty_launch cfg{launch_cfg ? launch_cfg->cols_per_block : 0, ln.waves, ln.groups};
+  const size_t need = celty_spmspv_batch_workspace_bytes(n, W);
   if (!workspace || misaligned(workspace, 256) || workspace_bytes < need) return CELTY_EINVAL;
 
-  KernelArgs a;
-  a.gptr = W->gptr;
-  a.values = reinterpret_cast<const uint4*>(W->values);
-  a.runs = W->runs;
-  a.x = static_cast<const unsigned short*>(x);
-  a.y = static_cast<unsigned short*>(y);
-  a.ws = static_cast<unsigned long long*>(workspace);
-  // merge scale: any row sum is at most K * max|w| * 65504 (the largest
-  // finite fp16 |x|); 2^s_glob maps that bound to at most 2^48
-  a.s_glob = 0;
-  {
-    const double bound = static_cast<double>(W->K) * static_cast<double>(W->max_abs) * 65504.0;
-    if (bound > 0.0) {
-      int e;
-      std::frexp(bound, &e);
-      a.s_glob = 48 - e;
+  BatchArgs ba{};
+  ba.n = n;
+  size_t ws_off = 0;
+  for (int i = 0; i < n; ++i) {
+    Plan pl;
+    if (celty_status st = make_plan(W[i], &cfg, pl)) return st;
+    void* ws_i = static_cast<unsigned char*>(workspace) + ws_off;
+    if (celty_status st = product_args(W[i], pl, x[i], tau[i], y[i], ws_i, ba.prod[i])) return st;
+    ws_off += celty_spmspv_workspace_bytes(W[i]->M, W[i]->K, W[i]->R);
+    ba.block_start[i] = static_cast<int>(ln.blocks);
+    ln.blocks += pl.blocks;
+    if (ln.blocks > 0x7FFFFFFF) return CELTY_EINVAL;
+    ln.lds = std::max(ln.lds, pl.lds);
+  }
+  ba.block_start[n] = static_cast<int>(ln.blocks);
+  // every y is written while the other products read their x; none may
+  // overlap another product's x or y, or the workspace
+  for (int i = 0; i < n; ++i) {
+    const size_t yb = 2u * static_cast<size_t>(W[i]->M);
+    if (overlaps(y[i], yb, workspace, need)) return CELTY_EINVAL;
+    if (overlaps(x[i], 2u * static_cast<size_t>(W[i]->K), workspace, need)) return CELTY_EINVAL;
+    for (int j = 0; j < n; ++j) {
+      if (j == i) continue;
+      if (overlaps(y[i], yb, x[j], 2u * static_cast<size_t>(W[j]->K))) return CELTY_EINVAL;
+      if (overlaps(y[i], yb, y[j], 2u * static_cast<size_t>(W[j]->M))) return CELTY_EINVAL;
     }
   }
-  a.tau = tau;
-  a.max_abs = W->max_abs;
-  a.n_groups = static_cast<uint32_t>(W->n_groups);
-  a.M = W->M;
-  a.K = W->K;
-  a.R = W->R;
-  a.Kc = pl.Kc;
-  a.KC = pl.KC;
-  a.tile_slots = pl.tile_slots;
-  a.seg_off = pl.seg_off;
-  a.scr_off = pl.scr_off;
-  a.misc_off = pl.misc_off;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  switch (pl.waves) {
-    case 2: return launch<2>(pl, a, s);
-    case 4: return launch<4>(pl, a, s);
-    case 8: return launch<8>(pl, a, s);
-    case 16: return launch<16>(pl, a, s);
-    default: return CELTY_EINVAL;
-  }
+  return launch(ln, ba, static_cast<hipStream_t>(stream));
 }
 
 extern "C" celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y, void* workspace,

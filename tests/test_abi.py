@@ -32,7 +32,8 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for want in ("celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv",
                  "celty_spmspv_ex", "celty_spmspv_plan", "celty_spmspv_workspace_bytes",
-                 "celty_spmspv_workspace_init", "celty_status_string", "celty_default_tile_rows"):
+                 "celty_spmspv_workspace_init", "celty_status_string", "celty_default_tile_rows",
+                 "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes"):
         assert want in names
 
 
@@ -230,6 +231,68 @@ def test_spmspv_rejects_bad_arguments(case):
         d.max_abs = -1.0
     pd = None if case == "null_desc" else ctypes.byref(d)
     st = celty._spmspv_ex(pd, x, tau, y, ws, nws, None if launch is None else ctypes.byref(launch), None)
+    assert st == CELTY_EINVAL
+
+
+def _batch_arrays(descs, xs, taus, ys):
+    n = len(descs)
+    arr = (ctypes.POINTER(celty_rlc_csc) * n)(*[ctypes.pointer(d) for d in descs])
+    return (arr, (ctypes.c_void_p * n)(*xs), (ctypes.c_float * n)(*taus), (ctypes.c_void_p * n)(*ys))
+
+
+def test_batch_workspace_bytes():
+    descs = [_desc(M=4096), _desc(M=1000, K=300, R=128), _desc(M=11008, R=1024)]
+    arr = (ctypes.POINTER(celty_rlc_csc) * 3)(*[ctypes.pointer(d) for d in descs])
+    want = sum(celty.celty_spmspv_workspace_bytes(d.M, d.K, d.R) for d in descs)
+    assert celty._batch_ws_bytes(3, arr) == want == 4096 * 8 + 8192 + 11008 * 8
+    assert celty._batch_ws_bytes(0, arr) == 0
+    assert celty._batch_ws_bytes(9, arr) == 0
+    assert celty._batch_ws_bytes(2, None) == 0
+
+
+@host_only
+@pytest.mark.parametrize("case", ["n0", "n9", "null_W", "null_x", "null_tau", "null_y", "bad_header",
+                                  "nan_tau", "y_over_other_x", "y_over_other_y", "y_over_ws", "x_over_ws",
+                                  "short_ws", "slices"])
+def test_batch_rejects_bad_arguments(case):
+    descs = [_desc(M=4096), _desc(M=1000, K=4096, R=128), _desc(M=2048, K=300, R=512)]
+    xs = [FAKE + 0x100000, FAKE + 0x100000, FAKE + 0x110000]      # products 0 and 1 share x
+    ys = [FAKE + 0x200000, FAKE + 0x210000, FAKE + 0x220000]
+    taus = [0.5, 0.5, 0.25]
+    ws = FAKE + 0x400000
+    n = 3
+    arr, xp, tp, yp = _batch_arrays(descs, xs, taus, ys)
+    nws = celty._batch_ws_bytes(n, arr)
+    launch = None
+    if case == "n0":
+        n = 0
+    elif case == "n9":
+        n = 9
+    elif case == "null_W":
+        arr = None
+    elif case == "null_x":
+        xp = None
+    elif case == "null_tau":
+        tp = None
+    elif case == "null_y":
+        yp = None
+    elif case == "bad_header":
+        descs[2].version = 2
+    elif case == "nan_tau":
+        tp[2] = math.nan
+    elif case == "y_over_other_x":
+        yp[0] = xs[2] + 64
+    elif case == "y_over_other_y":
+        yp[2] = ys[1] + 100
+    elif case == "y_over_ws":
+        yp[1] = ws + 256
+    elif case == "x_over_ws":
+        xp[2] = ws + 512
+    elif case == "short_ws":
+        nws -= 1
+    elif case == "slices":
+        launch = celty_launch(32, 4)                                  # 128 slices of 4096 columns
+    st = celty._batch(n, arr, xp, tp, yp, ws, nws, None if launch is None else ctypes.byref(launch), None)
     assert st == CELTY_EINVAL
 
 

@@ -246,3 +246,127 @@ def test_config5_projections(celty, torch_dev, as_):
         p = workloads.make_problem(5, proj.M, proj.K, c["ws"], as_, c["xdist"], seed=0, layer=0,
                                    proj=workloads.PROJ_IDS[name], x=x)
         _full(celty, torch_dev, p, f"config5 as{as_} {name}")
+
+
+# --------------------------------------------------------------------------
+# several products in one launch
+# --------------------------------------------------------------------------
+def _batch_run(celty, torch_dev, probs, Rs, launch=None, shared_x=False):
+    """Runs the products in one celty_spmspv_batch and, one by one, through
+    celty_spmspv_ex with the same launch; returns both results."""
+    torch, dev = torch_dev
+    encs = [celty.celty_encode(p.W, p.mask, R) for p, R in zip(probs, Rs)]
+    Wd = [e.to_device(dev) for e in encs]
+    xt = [torch.from_numpy(np.ascontiguousarray(p.x).view(np.int16)).to(dev) for p in probs]
+    if shared_x:
+        xt = [xt[0]] * len(probs)
+    ys = [torch.full((p.W.shape[0],), 0x7C01, dtype=torch.int16, device=dev) for p in probs]
+    ws = celty.new_batch_workspace(Wd, dev)
+    celty.celty_spmspv_batch(Wd, xt, [p.tau for p in probs], ys, ws, launch)
+    torch.cuda.synchronize()
+    assert int(ws.count_nonzero()) == 0, "batch workspace not left zero-filled"
+    singles = []
+    for W, x, p in zip(Wd, xt, probs):
+        y = torch.empty(p.W.shape[0], dtype=torch.int16, device=dev)
+        w1 = celty.new_workspace(W, dev)
+        celty.celty_spmspv_ex(W, x, p.tau, y, w1, launch)
+        singles.append(y)
+    torch.cuda.synchronize()
+    return ([y.cpu().numpy().view(np.float16) for y in ys], [y.cpu().numpy().view(np.float16) for y in singles])
+
+
+def _batch_launch_for(celty, probs, Rs, launch):
+    """The launch the batch resolves to, made explicit for the single calls
+    (the batch takes 16 wavefronts if any product has R >= 1024)."""
+    if launch is not None and len(launch) >= 2 and launch[1]:
+        return launch
+    waves = 16 if any(R >= 1024 for R in Rs) else 8
+    cols = launch[0] if launch else 0
+    groups = launch[2] if launch and len(launch) > 2 else 0
+    return (cols, waves, groups)
+
+
+@pytest.mark.parametrize("launch", [None, (256, 4, 1), (128, 8, 2)])
+def test_batch_shared_x(celty, torch_dev, launch):
+    _note(f"batch shared x launch={launch}")
+    K = 1500
+    p0 = workloads.random_small(501, 700, K, ws=60, as_=50)
+    probs = [p0] + [workloads.random_small(502 + i, M, K, ws=ws, as_=50) for i, (M, ws) in
+                    enumerate([(2049, 50), (3000, 70)])]
+    probs = [workloads.Problem(p.W, p.mask, p0.x, p0.tau, p.meta) for p in probs]
+    Rs = [256, 512, 128]
+    L = _batch_launch_for(celty, probs, Rs, launch)
+    yb, ys = _batch_run(celty, torch_dev, probs, Rs, L, shared_x=True)
+    for p, a, b in zip(probs, yb, ys):
+        _check(a, p.W, p.mask, p.x, p.tau)
+        assert np.array_equal(a.view(np.uint16), b.view(np.uint16)), "batch differs from single calls"
+
+
+def test_batch_independent_mixed_shapes(celty, torch_dev):
+    # different K, x and tau per product: one slice (K small), a tall tile,
+    # an all-inactive x, an empty matrix and an identity
+    _note("batch independent mixed shapes")
+    probs = [workloads.random_small(601, 3000, 40, ws=50, as_=50),
+             workloads.random_small(602, 5000, 2500, ws=70, as_=60),
+             workloads.random_small(603, 1000, 900, ws=50, as_=50),
+             workloads.random_small(604, 257, 129, ws=0, as_=0)]
+    probs[2] = workloads.Problem(probs[2].W, probs[2].mask, probs[2].x,
+                                 float(np.max(np.abs(probs[2].x.astype(np.float32)))), probs[2].meta)
+    I = np.eye(600, dtype=np.float16)
+    xi = np.random.default_rng(605).laplace(size=600).astype(np.float16)
+    probs.append(workloads.Problem(I, None, xi, 0.8, {}))
+    probs.append(workloads.Problem(np.zeros((300, 200), np.float16), None, np.ones(200, np.float16), -1.0, {}))
+    Rs = [256, 1024, 256, 64, 128, 64]
+    L = _batch_launch_for(celty, probs, Rs, None)
+    yb, ys = _batch_run(celty, torch_dev, probs, Rs, L)
+    for p, a, b in zip(probs, yb, ys):
+        _check(a, p.W, p.mask, p.x, p.tau)
+        assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+    assert np.all(yb[2].view(np.uint16) == 0)
+    assert np.all(yb[5].view(np.uint16) == 0)
+    want = np.where(np.abs(xi.astype(np.float32)) > 0.8, xi, np.float16(0)).astype(np.float16)
+    assert np.array_equal(yb[4].view(np.uint16), want.view(np.uint16))
+
+
+def test_batch_of_eight_repeated(celty, torch_dev):
+    torch, dev = torch_dev
+    _note("batch of eight, repeated")
+    probs = [workloads.random_small(700 + i, 300 + 250 * i, 800 + 97 * i, ws=50, as_=50) for i in range(8)]
+    Rs = [128, 256] * 4
+    encs = [celty.celty_encode(p.W, p.mask, R) for p, R in zip(probs, Rs)]
+    Wd = [e.to_device(dev) for e in encs]
+    xt = [torch.from_numpy(p.x.view(np.int16)).to(dev) for p in probs]
+    ws = celty.new_batch_workspace(Wd, dev)
+    outs = []
+    for rep in range(3):
+        ys = [torch.empty(p.W.shape[0], dtype=torch.int16, device=dev) for p in probs]
+        celty.celty_spmspv_batch(Wd, xt, [p.tau for p in probs], ys, ws)
+        outs.append(ys)
+    torch.cuda.synchronize()
+    assert int(ws.count_nonzero()) == 0
+    for ys in outs:
+        for p, y in zip(probs, ys):
+            _check(y.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
+
+
+def test_config3_layer_batched(celty, torch_dev):
+    # the 7B layer as four launches: q/k/v on one x, o, gate/up on one x, down
+    torch, dev = torch_dev
+    from paper_2608_01536_amd import default_tile_rows
+    probs = {p.meta['proj_name']: p for p in workloads.layer_problems(3, 0, 0)}
+    for group in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",)):
+        _note(f"config3 batched {group}")
+        ps = [probs[g] for g in group]
+        Rs = [default_tile_rows(*p.W.shape) for p in ps]
+        encs = [celty.celty_encode(p.W, p.mask, R) for p, R in zip(ps, Rs)]
+        Wd = [e.to_device(dev) for e in encs]
+        x = torch.from_numpy(ps[0].x.view(np.int16)).to(dev)
+        for p in ps[1:]:
+            assert np.array_equal(p.x.view(np.uint16), ps[0].x.view(np.uint16)) and p.tau == ps[0].tau
+        ys = [torch.empty(p.W.shape[0], dtype=torch.int16, device=dev) for p in ps]
+        ws = celty.new_batch_workspace(Wd, dev)
+        celty.celty_spmspv_batch(Wd, [x] * len(ps), [p.tau for p in ps], ys, ws)
+        torch.cuda.synchronize()
+        for p, y in zip(ps, ys):
+            err = _check(y.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
+            _note(f"  {p.meta['proj_name']} rel_err={err:.3e}")
