@@ -207,6 +207,35 @@ def sequence_bench(args) -> int:
     return 0
 
 
+def format_study(args) -> int:
+    """Host only: stored size of a 4096x4096 fp16 matrix in this library's
+    RLC-CSC (4-bit runs, Section 3.2) against a bitmap format and dense fp16,
+    across weight sparsity (the paper's compression-efficiency comparison).
+    RLC-CSC is counted three ways: 2.5 B per stored entry (values + runs, the
+    paper's accounting), plus the 8-entry alignment of each segment, plus the
+    group pointers.  The bitmap is its theoretical size: one bit per position
+    and 2 B per non-zero."""
+    import paper_2608_01536_amd as celty
+    import workloads
+
+    M = K = 4096
+    dense = 2 * M * K
+    rows = []
+    for ws in (10, 20, 30, 40, 50, 60, 70, 80, 90):
+        p = workloads.make_problem(2, M, K, ws, 50, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
+        for R in ([512, 4096] if ws in (50, 70) else [512]):
+            enc = celty.celty_encode(p.W, p.mask, R)
+            entries = 2.5 * (enc.n_nnz + enc.n_pad)
+            aligned = 2 * 8 * enc.n_groups + 4 * enc.n_groups
+            stored = aligned + 4 * (enc.T * K + 1)
+            bitmap = M * K / 8.0 + 2.0 * enc.n_nnz
+            rows.append({"weight_sparsity_pct": ws, "R": R, "nnz": int(enc.n_nnz), "padding": int(enc.n_pad),
+                         "rlc_entry_ratio": round(entries / dense, 4), "rlc_aligned_ratio": round(aligned / dense, 4),
+                         "rlc_stored_ratio": round(stored / dense, 4), "bitmap_ratio": round(bitmap / dense, 4)})
+            print(json.dumps(rows[-1]), flush=True)
+    return 0
+
+
 def copy_calibration() -> int:
     """A plain device copy of CALIBRATION_BYTES (reads and writes that many
     bytes once): run under the FETCH_SIZE / WRITE_SIZE counters to scale them."""
@@ -334,9 +363,13 @@ def main() -> int:
                     help="time one decode step of config 3, 4 or 5 (its own JSON line)")
     ap.add_argument("--layers", type=int, default=0, help="layers of --sequence (0 = the config's)")
     ap.add_argument("--seq-as", type=float, default=None, help="activation sparsity of --sequence")
+    ap.add_argument("--format-study", action="store_true",
+                    help="host only: RLC-CSC vs bitmap vs dense sizes across weight sparsity")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration()
+    if args.format_study:
+        return format_study(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the SpMSpV path here is single-GPU "

@@ -404,25 +404,20 @@ struct KernelArgs {
   int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS (the tile is at 0)
 };
 
-// Up to kMaxBatch independent products in one launch: product i owns
-// workgroups [block_start[i], block_start[i + 1]).
+// Up to kMaxBatch independent products in one launch: grid (max blocks, n),
+// product blockIdx.y owns workgroups blockIdx.x < blocks[blockIdx.y].  (The
+// product is found from the block index alone, so its arguments arrive with
+// one scalar load latency, as for a single product.)
 constexpr int kMaxBatch = 8;
 struct BatchArgs {
-  int n;
-  int block_start[kMaxBatch + 1];
+  int blocks[kMaxBatch];
   KernelArgs prod[kMaxBatch];
 };
 
+// One workgroup's share of product p: row tile and column slice number blk.
 template <int WAVES, int G, int DEPTH>
-__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(BatchArgs ba) {
+__device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
   constexpr int NT = WAVES * kWave;
-  // this workgroup's product (workgroup-uniform) and its index within it
-  int pi = 0;
-#pragma unroll
-  for (int i = 1; i < kMaxBatch; ++i)
-    pi = (i < ba.n && static_cast<int>(blockIdx.x) >= ba.block_start[i]) ? i : pi;
-  const KernelArgs& p = ba.prod[pi];
-  const int blk = static_cast<int>(blockIdx.x) - ba.block_start[pi];
   extern __shared__ __align__(16) unsigned char smem[];
   int* tile = reinterpret_cast<int*>(smem);
   // the tile's LDS byte address (for the accumulation's own LDS instructions)
@@ -602,6 +597,18 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(BatchArgs ba) {
   }
 }
 
+template <int WAVES, int G, int DEPTH>
+__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
+  spmspv_block<WAVES, G, DEPTH>(p, static_cast<int>(blockIdx.x));
+}
+
+template <int WAVES, int G, int DEPTH>
+__global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs ba) {
+  const int pi = static_cast<int>(blockIdx.y);
+  if (static_cast<int>(blockIdx.x) >= ba.blocks[pi]) return;   // past this product's grid
+  spmspv_block<WAVES, G, DEPTH>(ba.prod[pi], static_cast<int>(blockIdx.x));
+}
+
 // Global selection: one workgroup of 1024 lanes walks x in 1024-wide steps;
 // ballot + mbcnt give each active lane its rank, wave totals are combined in
 // LDS, and indices are written in ascending order.
@@ -707,24 +714,36 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   return CELTY_OK;
 }
 
-// The launch: total workgroups and the largest LDS footprint of the batch.
+// The launch: products, the largest per-product grid and LDS footprint.
 struct Launch {
-  int waves = 8, groups = 1;
-  int64_t blocks = 0;
+  int waves = 8, groups = 1, n = 0;
+  int64_t max_blocks = 0;
   size_t lds = 0;
 };
 
+// Lets a kernel take more than 64 KB of dynamic LDS (once per kernel).
+template <typename F>
+bool allow_large_lds(F* fn, bool& done) {
+  if (done) return true;
+  done = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             kMaxLds) == hipSuccess;
+  return done;
+}
+
 template <int WAVES, int G, int DEPTH>
 celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
-  static bool attr_set = false;
-  if (ln.lds > 64 * 1024 && !attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&spmspv_kernel<WAVES, G, DEPTH>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds) != hipSuccess)
+  static bool single_attr = false, batch_attr = false;
+  if (ln.n == 1) {
+    if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_kernel<WAVES, G, DEPTH>, single_attr)) return CELTY_EHIP;
+    hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.max_blocks)),
+                       dim3(WAVES * kWave), ln.lds, stream, a.prod[0]);
+  } else {
+    if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_batch_kernel<WAVES, G, DEPTH>, batch_attr))
       return CELTY_EHIP;
-    attr_set = true;
+    hipLaunchKernelGGL((spmspv_batch_kernel<WAVES, G, DEPTH>),
+                       dim3(static_cast<unsigned>(ln.max_blocks), static_cast<unsigned>(ln.n)),
+                       dim3(WAVES * kWave), ln.lds, stream, a);
   }
-  hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.blocks)), dim3(WAVES * kWave),
-                     ln.lds, stream, a);
   return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
 }
 
@@ -864,7 +883,7 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
   if (!workspace || misaligned(workspace, 256) || workspace_bytes < need) return CELTY_EINVAL;
 
   BatchArgs ba{};
-  ba.n = n;
+  ln.n = n;
   size_t ws_off = 0;
   for (int i = 0; i < n; ++i) {
     Plan pl;
@@ -872,12 +891,10 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
     void* ws_i = static_cast<unsigned char*>(workspace) + ws_off;
     if (celty_status st = product_args(W[i], pl, x[i], tau[i], y[i], ws_i, ba.prod[i])) return st;
     ws_off += celty_spmspv_workspace_bytes(W[i]->M, W[i]->K, W[i]->R);
-    ba.block_start[i] = static_cast<int>(ln.blocks);
-    ln.blocks += pl.blocks;
-    if (ln.blocks > 0x7FFFFFFF) return CELTY_EINVAL;
+    ba.blocks[i] = static_cast<int>(pl.blocks);   // make_plan keeps it below 2^31
+    ln.max_blocks = std::max(ln.max_blocks, pl.blocks);
     ln.lds = std::max(ln.lds, pl.lds);
   }
-  ba.block_start[n] = static_cast<int>(ln.blocks);
   // every y is written while the other products read their x; none may
   // overlap another product's x or y, or the workspace
   for (int i = 0; i < n; ++i) {
