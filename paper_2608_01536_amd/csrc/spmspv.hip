@@ -32,6 +32,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <type_traits>
 #include <cmath>
 #include <cstdint>
 
@@ -577,24 +578,51 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
   constexpr long long kBias = 1ll << 49;
   constexpr unsigned long long kCount = 1ull << 56;
   const int shift = p.s_glob - scale;
-  for (int r = tid; r < rows; r += NT) {
-    const long long q = tile[r];
-    long long v;
-    if (shift >= 0) {
-      v = q * (1ll << shift);
-    } else {   // round half up onto the coarser grid
-      const int rs = -shift;
-      v = rs > 62 ? 0 : ((q + (1ll << (rs - 1))) >> rs);
-    }
-    const unsigned long long ticket = kCount + static_cast<unsigned long long>(v + kBias);
-    const unsigned long long old = atomicAdd(p.ws + row0 + r, ticket);
+  const auto fixed_at_launch_scale = [&](long long q) -> long long {
+    if (shift >= 0) return q * (1ll << shift);
+    const int rs = -shift;   // round half up onto the coarser grid
+    return rs > 62 ? 0 : ((q + (1ll << (rs - 1))) >> rs);
+  };
+  const auto finish_row = [&](int r, unsigned long long ticket, unsigned long long old) {
     if ((old >> 56) == static_cast<unsigned long long>(p.KC - 1)) {
       const long long total = static_cast<long long>((old & (kCount - 1)) + (ticket & (kCount - 1))) -
                               static_cast<long long>(p.KC) * kBias;
       p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(total), -p.s_glob));
       p.ws[row0 + r] = 0ull;
     }
+  };
+  if (rows <= NT) {   // workgroup-uniform: one row per lane
+    if (tid < rows) {
+      const unsigned long long ticket = kCount + static_cast<unsigned long long>(fixed_at_launch_scale(tile[tid]) + kBias);
+      finish_row(tid, ticket, atomicAdd(p.ws + row0 + tid, ticket));
+    }
+    return;
   }
+  // Taller tiles: a lane's rows go J at a time (J = 2 up to twice the
+  // workgroup's lanes, else 4), their atomics issued back to back (a row past
+  // the tile adds a zero ticket to slot 0 of the tile, which changes nothing,
+  // so no branch separates them), then their returns are examined.
+  const auto merge_rows = [&](auto in_flight) {
+    constexpr int J = decltype(in_flight)::value;
+    for (int r0 = tid; r0 < rows; r0 += J * NT) {
+      unsigned long long ticket[J], old[J];
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int r = r0 + j * NT;
+        const bool in = r < rows;
+        ticket[j] = in ? kCount + static_cast<unsigned long long>(fixed_at_launch_scale(tile[in ? r : 0]) + kBias)
+                       : 0ull;
+        old[j] = atomicAdd(p.ws + row0 + (in ? r : 0), ticket[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        if (r0 + j * NT < rows) finish_row(r0 + j * NT, ticket[j], old[j]);
+    }
+  };
+  if (rows <= 2 * NT)
+    merge_rows(std::integral_constant<int, 2>{});
+  else
+    merge_rows(std::integral_constant<int, 4>{});
 }
 
 template <int WAVES, int G, int DEPTH>
