@@ -415,9 +415,21 @@ struct BatchArgs {
   KernelArgs prod[kMaxBatch];
 };
 
+// The arguments the first loads of a workgroup need.  A single-product
+// launch passes them as leading kernel arguments, which gfx950 preloads into
+// scalar registers at dispatch (the library is built with
+// -amdgpu-kernarg-preload-count), so a workgroup's first memory round trip
+// does not wait for its argument block to be fetched.
+struct Early {
+  const uint32_t* gptr;
+  const unsigned short* x;
+  int K, Kc, KC;
+  float tau;
+};
+
 // One workgroup's share of product p: row tile and column slice number blk.
 template <int WAVES, int G, int DEPTH>
-__device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
+__device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p, int blk) {
   constexpr int NT = WAVES * kWave;
   extern __shared__ __align__(16) unsigned char smem[];
   int* tile = reinterpret_cast<int*>(smem);
@@ -430,7 +442,7 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
   int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const int t = blk / p.KC, c = blk - t * p.KC;
+  const int t = blk / e.KC, c = blk - t * e.KC;
   const int row0 = t * p.R;
   const int rows = min(p.R, p.M - row0);
   const int base4_cap = 4 * (p.R + 7);   // tile byte address cap of a group base
@@ -444,9 +456,9 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
   // The flat group sequence is then cut into one range per wavefront:
   // segment i goes to wavefront wave_of(off_i), and wfirst[w] collects the
   // lowest segment index of wavefront w (INT_MAX when none starts there).
-  const int k0 = c * p.Kc;
-  const int kn = min(p.Kc, p.K - k0);
-  const uint32_t* gp = p.gptr + static_cast<size_t>(t) * p.K + k0;
+  const int k0 = c * e.Kc;
+  const int kn = min(e.Kc, e.K - k0);
+  const uint32_t* gp = e.gptr + static_cast<size_t>(t) * e.K + k0;
   uint32_t n_seg, n_grp;
   if (kn <= NT) {
     // one column per lane
@@ -454,10 +466,10 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
     if (tid < kn) {
       g0 = gp[tid];
       g1 = gp[tid + 1];
-      xr = p.x[k0 + tid];
+      xr = e.x[k0 + tid];
     }
     const float xv = half_bits_to_float(xr);
-    const bool keep = tid < kn && fabsf(xv) > p.tau && g1 > g0;
+    const bool keep = tid < kn && fabsf(xv) > e.tau && g1 > g0;
     const uint32_t cnt = keep ? g1 - g0 : 0u;
     // |x| >= 0 orders like its bit pattern
     uint32_t en, eg, xmax_bits;
@@ -482,12 +494,12 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
 #pragma unroll
     for (int j = 0; j <= kMaxCols; ++j) g[j] = gp[min(kb + j, kn)];
 #pragma unroll
-    for (int j = 0; j < kMaxCols; ++j) xr[j] = p.x[k0 + min(kb + j, kn - 1)];
+    for (int j = 0; j < kMaxCols; ++j) xr[j] = e.x[k0 + min(kb + j, kn - 1)];
     uint32_t keep_bits = 0u, n_loc = 0u, g_loc = 0u, m_loc = 0u;
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) {
       const float xv = half_bits_to_float(xr[j]);
-      const bool keep = j < m && kb + j < kn && fabsf(xv) > p.tau && g[j + 1] > g[j];
+      const bool keep = j < m && kb + j < kn && fabsf(xv) > e.tau && g[j + 1] > g[j];
       keep_bits |= (keep ? 1u : 0u) << j;
       n_loc += keep ? 1u : 0u;
       g_loc += keep ? g[j + 1] - g[j] : 0u;
@@ -563,7 +575,7 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
   __syncthreads();
 
   // ---- merge --------------------------------------------------------------
-  if (p.KC == 1) {
+  if (e.KC == 1) {
     for (int r = tid; r < rows; r += NT)
       p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -scale));
     return;
@@ -584,9 +596,9 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
     return rs > 62 ? 0 : ((q + (1ll << (rs - 1))) >> rs);
   };
   const auto finish_row = [&](int r, unsigned long long ticket, unsigned long long old) {
-    if ((old >> 56) == static_cast<unsigned long long>(p.KC - 1)) {
+    if ((old >> 56) == static_cast<unsigned long long>(e.KC - 1)) {
       const long long total = static_cast<long long>((old & (kCount - 1)) + (ticket & (kCount - 1))) -
-                              static_cast<long long>(p.KC) * kBias;
+                              static_cast<long long>(e.KC) * kBias;
       p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(total), -p.s_glob));
       p.ws[row0 + r] = 0ull;
     }
@@ -626,15 +638,17 @@ __device__ __forceinline__ void spmspv_block(const KernelArgs& p, int blk) {
 }
 
 template <int WAVES, int G, int DEPTH>
-__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(KernelArgs p) {
-  spmspv_block<WAVES, G, DEPTH>(p, static_cast<int>(blockIdx.x));
+__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(const uint32_t* gptr, const unsigned short* x, int K,
+                                                                int Kc, int KC, float tau, KernelArgs p) {
+  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, K, Kc, KC, tau}, p, static_cast<int>(blockIdx.x));
 }
 
 template <int WAVES, int G, int DEPTH>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs ba) {
   const int pi = static_cast<int>(blockIdx.y);
   if (static_cast<int>(blockIdx.x) >= ba.blocks[pi]) return;   // past this product's grid
-  spmspv_block<WAVES, G, DEPTH>(ba.prod[pi], static_cast<int>(blockIdx.x));
+  const KernelArgs& p = ba.prod[pi];
+  spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.K, p.Kc, p.KC, p.tau}, p, static_cast<int>(blockIdx.x));
 }
 
 // Global selection: one workgroup of 1024 lanes walks x in 1024-wide steps;
@@ -763,8 +777,9 @@ celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stre
   static bool single_attr = false, batch_attr = false;
   if (ln.n == 1) {
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_kernel<WAVES, G, DEPTH>, single_attr)) return CELTY_EHIP;
+    const KernelArgs& q = a.prod[0];
     hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.max_blocks)),
-                       dim3(WAVES * kWave), ln.lds, stream, a.prod[0]);
+                       dim3(WAVES * kWave), ln.lds, stream, q.gptr, q.x, q.K, q.Kc, q.KC, q.tau, q);
   } else {
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_batch_kernel<WAVES, G, DEPTH>, batch_attr))
       return CELTY_EHIP;
