@@ -370,3 +370,81 @@ def test_config3_layer_batched(celty, torch_dev):
         for p, y in zip(ps, ys):
             err = _check(y.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
             _note(f"  {p.meta['proj_name']} rel_err={err:.3e}")
+
+
+# --------------------------------------------------------------------------
+# graph capture, concurrent streams, very wide K
+# --------------------------------------------------------------------------
+def test_graph_replays_match_eager(celty, torch_dev):
+    # one single-product call and one batch captured in a HIP graph, replayed
+    # several times with eager work between replays; every replay must equal
+    # the eager result bit for bit and leave the workspaces zero
+    torch, dev = torch_dev
+    _note("graph replays")
+    p = workloads.random_small(801, 2500, 3000, ws=60, as_=50)
+    q = workloads.random_small(802, 1200, 3000, ws=50, as_=50)
+    Wp = celty.celty_encode(p.W, p.mask, 512).to_device(dev)
+    Wq = celty.celty_encode(q.W, q.mask, 256).to_device(dev)
+    xp = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    xq = torch.from_numpy(q.x.view(np.int16)).to(dev)
+    ws1 = celty.new_workspace(Wp, dev)
+    wsb = celty.new_batch_workspace([Wp, Wq], dev)
+    y1 = torch.empty(2500, dtype=torch.int16, device=dev)
+    yb = [torch.empty(2500, dtype=torch.int16, device=dev), torch.empty(1200, dtype=torch.int16, device=dev)]
+    e1 = torch.empty_like(y1)
+    eb = [torch.empty_like(t) for t in yb]
+    celty.celty_spmspv(Wp, xp, p.tau, e1, ws1)
+    celty.celty_spmspv_batch([Wp, Wq], [xp, xq], [p.tau, q.tau], eb, wsb)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        celty.celty_spmspv(Wp, xp, p.tau, y1, ws1)
+        celty.celty_spmspv_batch([Wp, Wq], [xp, xq], [p.tau, q.tau], yb, wsb)
+    for rep in range(4):
+        for t in [y1] + yb:
+            t.fill_(0x7C01)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y1, e1), f"replay {rep}: single product differs"
+        assert all(torch.equal(a, b) for a, b in zip(yb, eb)), f"replay {rep}: batch differs"
+        assert int(ws1.count_nonzero()) == 0 and int(wsb.count_nonzero()) == 0
+        celty.celty_spmspv(Wq, xq, q.tau, yb[1], celty.new_workspace(Wq, dev))   # eager work between replays
+        torch.cuda.synchronize()
+    _check(e1.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
+
+
+def test_two_streams_with_own_workspaces(celty, torch_dev):
+    torch, dev = torch_dev
+    _note("two streams")
+    probs = [workloads.random_small(811 + i, 3000, 2000, ws=50, as_=50) for i in range(2)]
+    Ws = [celty.celty_encode(p.W, p.mask, 512).to_device(dev) for p in probs]
+    xs = [torch.from_numpy(p.x.view(np.int16)).to(dev) for p in probs]
+    wss = [celty.new_workspace(W, dev) for W in Ws]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[], []]
+    for rep in range(6):
+        for i in range(2):
+            with torch.cuda.stream(streams[i]):
+                y = torch.empty(3000, dtype=torch.int16, device=dev)
+                celty.celty_spmspv(Ws[i], xs[i], probs[i].tau, y, wss[i])
+                outs[i].append(y)
+    torch.cuda.synchronize()
+    for i in range(2):
+        assert int(wss[i].count_nonzero()) == 0
+        first = outs[i][0].cpu()
+        _check(first.numpy().view(np.float16), probs[i].W, probs[i].mask, probs[i].x, probs[i].tau)
+        for y in outs[i][1:]:
+            assert torch.equal(y.cpu(), first)
+
+
+def test_very_wide_K_automatic_shape(celty, torch_dev):
+    # K = 100000 puts more than one column on each selection lane under the
+    # automatic shape (slices of ~1600 columns, at most 63 slices)
+    torch, dev = torch_dev
+    p = workloads.random_small(821, 300, 100000, ws=80, as_=60)
+    enc = celty.celty_encode(p.W, p.mask, 256)
+    plan = celty.celty_spmspv_plan(enc, None)
+    _note(f"very wide K plan {plan}")
+    assert plan['cols_per_block'] > 64 * plan['waves_per_block']
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, 256, enc=enc)
+    _check(y, p.W, p.mask, p.x, p.tau)
