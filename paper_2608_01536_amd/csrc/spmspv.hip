@@ -31,6 +31,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <type_traits>
 #include <cmath>
@@ -763,18 +764,25 @@ struct Launch {
   size_t lds = 0;
 };
 
-// Lets a kernel take more than 64 KB of dynamic LDS (once per kernel).
+// Lets a kernel take more than 64 KB of dynamic LDS on the current device
+// (once per kernel and device: `done` holds one bit per device id below 64;
+// setting the attribute again is harmless, so two threads racing here are).
 template <typename F>
-bool allow_large_lds(F* fn, bool& done) {
-  if (done) return true;
-  done = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
-                             kMaxLds) == hipSuccess;
-  return done;
+bool allow_large_lds(F* fn, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  const uint64_t bit = dev < 64 ? (1ull << dev) : 0ull;
+  if (bit && (done.load(std::memory_order_relaxed) & bit)) return true;
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds) !=
+      hipSuccess)
+    return false;
+  done.fetch_or(bit, std::memory_order_relaxed);
+  return true;
 }
 
 template <int WAVES, int G, int DEPTH>
 celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
-  static bool single_attr = false, batch_attr = false;
+  static std::atomic<uint64_t> single_attr{0}, batch_attr{0};
   if (ln.n == 1) {
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_kernel<WAVES, G, DEPTH>, single_attr)) return CELTY_EHIP;
     const KernelArgs& q = a.prod[0];

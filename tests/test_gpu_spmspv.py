@@ -448,3 +448,20 @@ def test_very_wide_K_automatic_shape(celty, torch_dev):
     assert plan['cols_per_block'] > 64 * plan['waves_per_block']
     y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, 256, enc=enc)
     _check(y, p.W, p.mask, p.x, p.tau)
+
+
+def test_tall_tile_needs_more_than_64kb_of_lds(celty, torch_dev):
+    # one tile of 30000 rows: about 120 KB of LDS, above the 64 KB default
+    torch, dev = torch_dev
+    p = workloads.random_small(831, 30000, 500, ws=70, as_=50)
+    enc = celty.celty_encode(p.W, p.mask, 30000)
+    plan = celty.celty_spmspv_plan(enc, None)
+    _note(f"tall tile plan {plan}")
+    assert plan['lds_bytes'] > 64 * 1024
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, 30000, enc=enc)
+    _check(y, p.W, p.mask, p.x, p.tau)
+    q = workloads.random_small(832, 700, 500, ws=50, as_=50)
+    yb, ys = _batch_run(celty, torch_dev, [p, q], [30000, 256], _batch_launch_for(celty, [p, q], [30000, 256], None))
+    for pr, a, b in zip([p, q], yb, ys):
+        _check(a, pr.W, pr.mask, pr.x, pr.tau)
+        assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
