@@ -236,6 +236,30 @@ def format_study(args) -> int:
     return 0
 
 
+def encode_throughput(args) -> int:
+    """Host only: throughput of the library's RLC-CSC encoder (offline in the
+    paper, Section 3.2) on the benchmark matrices, in dense entries scanned
+    and stored entries written per second, for several thread counts."""
+    import paper_2608_01536_amd as celty
+    import workloads
+
+    cpus = len(os.sched_getaffinity(0))
+    for (M, K, ws) in ((4096, 4096, 70), (4096, 4096, 50), (28672, 8192, 50)):
+        p = workloads.make_problem(2, M, K, ws, 50, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
+        R = celty.default_tile_rows(M, K)
+        for threads in sorted({1, 4, cpus}):
+            best = float("inf")
+            for _ in range(3):
+                t = time.perf_counter()
+                enc = celty.celty_encode(p.W, p.mask, R, n_threads=threads)
+                best = min(best, time.perf_counter() - t)
+            print(json.dumps({"M": M, "K": K, "weight_sparsity_pct": ws, "R": R, "threads": threads,
+                              "seconds": round(best, 4), "dense_entries_per_s": round(M * K / best / 1e6, 1),
+                              "stored_entries_per_s": round(enc.n_entries / best / 1e6, 1),
+                              "unit": "millions per second", "host_cpus": cpus}), flush=True)
+    return 0
+
+
 def copy_calibration() -> int:
     """A plain device copy of CALIBRATION_BYTES (reads and writes that many
     bytes once): run under the FETCH_SIZE / WRITE_SIZE counters to scale them."""
@@ -376,11 +400,15 @@ def main() -> int:
     ap.add_argument("--seq-as", type=float, default=None, help="activation sparsity of --sequence")
     ap.add_argument("--format-study", action="store_true",
                     help="host only: RLC-CSC vs bitmap vs dense sizes across weight sparsity")
+    ap.add_argument("--encode-throughput", action="store_true",
+                    help="host only: encoder throughput on the benchmark matrices")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration()
     if args.format_study:
         return format_study(args)
+    if args.encode_throughput:
+        return encode_throughput(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the SpMSpV path here is single-GPU "
