@@ -465,3 +465,52 @@ def test_tall_tile_needs_more_than_64kb_of_lds(celty, torch_dev):
     for pr, a, b in zip([p, q], yb, ys):
         _check(a, pr.W, pr.mask, pr.x, pr.tau)
         assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+
+
+# --------------------------------------------------------------------------
+# numerical edge cases of x, tau and the weights
+# --------------------------------------------------------------------------
+def test_nan_x_is_never_active_and_inf_tau_selects_nothing(celty, torch_dev):
+    p = workloads.random_small(841, 1500, 900, ws=50, as_=30)
+    x = p.x.copy()
+    rng = np.random.default_rng(841)
+    x[rng.random(x.size) < 0.1] = np.float16(np.nan)
+    _note("nan x")
+    y = _run(celty, torch_dev, p.W, p.mask, x, p.tau, 256)
+    _check(y, p.W, p.mask, x, p.tau)
+    _note("tau = +inf")
+    y = _run(celty, torch_dev, p.W, p.mask, x, float("inf"), 256)
+    assert np.all(y.view(np.uint16) == 0)
+
+
+def test_signed_zero_and_subnormal_activations(celty, torch_dev):
+    # tau = 0: +-0 is inactive, every subnormal is active; the products are
+    # ~1e-4, so the workgroups pick a large fixed-point scale.  (The weights
+    # are scaled so that y stays in fp16's normal range: for subnormal outputs
+    # the fp16 rounding of y alone, 2^-24 absolute, exceeds 2e-3 of max|y|.)
+    rng = np.random.default_rng(851)
+    M, K = 2000, 700
+    W = (rng.standard_normal((M, K)) * 30).astype(np.float16)
+    mask = (rng.random((M, K)) < 0.5).astype(np.uint8)
+    bits = rng.integers(1, 0x03FF, size=K).astype(np.uint16)            # subnormal magnitudes
+    bits |= (rng.integers(0, 2, size=K).astype(np.uint16) << np.uint16(15))
+    bits[rng.random(K) < 0.2] = 0x0000
+    bits[rng.random(K) < 0.1] = 0x8000
+    x = bits.view(np.float16)
+    _note("subnormal x")
+    y = _run(celty, torch_dev, W, mask, x, 0.0, 256)
+    _check(y, W, mask, x, 0.0)
+
+
+def test_large_weights_and_activations(celty, torch_dev):
+    # weights up to ~16 and activations up to ~1000: outputs of several
+    # thousand, within fp16 range; the scales adapt to max|w| and max|x|
+    rng = np.random.default_rng(861)
+    M, K = 1800, 600
+    W = (rng.standard_normal((M, K)) * 4).astype(np.float16)
+    mask = (rng.random((M, K)) < 0.3).astype(np.uint8)
+    x = (rng.laplace(size=K) * 100).astype(np.float16)
+    tau = workloads.tau_for_sparsity(x, 50)
+    _note("large magnitudes")
+    y = _run(celty, torch_dev, W, mask, x, tau, 512)
+    _check(y, W, mask, x, tau)
