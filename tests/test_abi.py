@@ -311,3 +311,31 @@ def test_single_hip_runtime_alongside_torch():
     import torch  # noqa: F401
     maps = {l.split()[-1] for l in open("/proc/self/maps") if "libamdhip64" in l}
     assert len(maps) == 1, maps
+
+
+def test_package_refuses_to_import_without_the_library(tmp_path):
+    """With libcelty.so absent the binding raises at import: there is no
+    fallback path to run instead of the HIP kernels."""
+    import shutil
+    pkg = os.path.join(ROOT, "paper_2608_01536_amd")
+    dst = tmp_path / "paper_2608_01536_amd"
+    dst.mkdir()
+    for name in os.listdir(pkg):
+        if name.endswith(".py"):
+            shutil.copy(os.path.join(pkg, name), dst / name)
+    env = dict(os.environ, PYTHONPATH=str(tmp_path))
+    res = subprocess.run(["python3", "-c", "import paper_2608_01536_amd"], cwd=str(tmp_path), env=env,
+                         stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    assert res.returncode != 0
+    assert "ImportError" in res.stderr and "is not built" in res.stderr
+
+
+def test_product_path_does_not_use_the_oracle():
+    """Neither the binding nor the native sources reference the CPU oracle."""
+    pkg = os.path.join(ROOT, "paper_2608_01536_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for name in files:
+            if name.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, name)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle\b", text, flags=re.M), name
+                assert "oracle/" not in text and "oracle." not in text, name
