@@ -298,6 +298,19 @@ def algorithmic_bytes_from_encoding(enc, x: np.ndarray, tau: float) -> tuple:
     return 2.5 * e_a + 2.0 * enc.K + 2.0 * enc.M, e_a, g_a
 
 
+def fetched_bytes_from_encoding(enc, g_a: int, plan: dict) -> tuple:
+    """Bytes the kernel's own loads and stores request (merge atomics aside).
+
+    compressed: every 8-entry group of an active column's segments (16 B of
+    values + 4 B of runs, the trailing alignment entries included) plus the
+    group pointers (each workgroup reads the Kc + 1 pointers of its slice in
+    its row tile, so T * (K + KC) words).  total adds x, read once per row tile
+    (2 B * T * K), and y (2 B * M).  Returns (compressed, total)."""
+    KC = -(-enc.K // plan["cols_per_block"])
+    compressed = 20 * g_a + 4 * enc.T * (enc.K + KC)
+    return compressed, compressed + 2 * enc.T * enc.K + 2 * enc.M
+
+
 def stored_bytes(enc) -> int:
     return 2 * enc.values.size + 4 * enc.runs.size + 4 * enc.gptr.size
 
@@ -336,6 +349,103 @@ def time_graph(torch, fn, steps: int, replays: int = 5) -> tuple:
         samples.append(s.elapsed_time(e) * 1e3 / steps)
     del g
     return float(np.median(samples)), samples
+
+
+def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool = False) -> dict:
+    """Graph-timed µs per celty_spmspv_ex call on rotated device copies of enc
+    (at least COLD_BYTES in all, so every call streams W from HBM)."""
+    dev = torch.device("cuda:0")
+    ncopies = 1 if hot else max(2, -(-COLD_BYTES // stored_bytes(enc)))
+    base = enc.to_device(dev)
+    copies = [base] + [base.clone_to() for _ in range(ncopies - 1)]
+    x = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    y = torch.empty(enc.M, dtype=torch.int16, device=dev)
+    ws = celty.new_workspace(base, dev)
+
+    def step(i):
+        # stream = None: the binding launches on torch's current stream, which
+        # is the capture stream while a graph is being recorded
+        celty.celty_spmspv_ex(copies[i % ncopies], x, p.tau, y, ws, launch)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    eager_us = time_loop(torch, step, steps)
+    # the timed region: the steps captured in one HIP graph and replayed on
+    # the launch stream; one step is exactly one kernel launch
+    us, samples = time_graph(torch, step, steps)
+    out = {"us": us, "samples": samples, "eager_us": eager_us, "copies": ncopies,
+           "y": y.cpu().numpy().view(np.float16)}
+    del copies, base
+    torch.cuda.empty_cache()
+    return out
+
+
+def cold_dense(torch, F, p, steps: int, hot: bool = False) -> dict:
+    """The dense reference: F.linear fp16 at batch 1 on the masked W and the
+    thresholded x, same cold rotation and graph timing."""
+    dev = torch.device("cuda:0")
+    M, K = p.W.shape
+    Wf = torch.from_numpy(np.where(p.mask != 0, p.W, np.float16(0))).to(dev)
+    nd = 1 if hot else max(2, -(-COLD_BYTES // (2 * M * K)))
+    dcopies = [Wf] + [Wf.clone() for _ in range(nd - 1)]
+    xd = torch.from_numpy(np.where(np.abs(p.x.astype(np.float32)) > p.tau, p.x, np.float16(0))).to(dev)[None]
+    for i in range(20):
+        F.linear(xd, dcopies[i % nd])
+    try:
+        dense_us, _ = time_graph(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps)
+        dense_mode = "graph"
+    except Exception:
+        dense_us, dense_mode = time_loop(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps), "eager"
+    del dcopies, Wf
+    torch.cuda.empty_cache()
+    return {"us": round(dense_us, 3), "GBps": round((2 * M * K + 2 * K + 2 * M) / dense_us / 1e3, 1),
+            "op": "torch.nn.functional.linear fp16, batch 1 (hipBLASLt/rocBLAS)", "copies": nd,
+            "timing": dense_mode}
+
+
+PAPER_SHAPES = ((4096, 4096), (4096, 11008), (5120, 5120), (5120, 13824), (7168, 7168), (7168, 28672))
+
+
+def paper_shapes(args) -> int:
+    """The six layer shapes of the paper's kernel evaluation (LLaMA-2-7B,
+    LLaMA-2-13B and OPT-30B projections, Section 5) at 30, 50 and 70 % dual
+    sparsity (weight = activation sparsity), each against the dense fp16
+    GEMV under the same cold protocol; one JSON line per point, then the mean
+    speedup per sparsity level (the paper reports its own means as context)."""
+    import torch
+    import torch.nn.functional as F
+
+    import paper_2608_01536_amd as celty
+    import workloads
+    from oracle import spmspv as ref
+
+    speed = {}
+    for pct in (30, 50, 70):
+        for (M, K) in PAPER_SHAPES:
+            p = workloads.make_problem(2, M, K, pct, pct, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
+            R = celty.default_tile_rows(M, K)
+            enc = celty.celty_encode(p.W, p.mask, R)
+            plan = celty.celty_spmspv_plan(enc, None)
+            b_alg, _, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
+            comp, _ = fetched_bytes_from_encoding(enc, g_a, plan)
+            sp_ = cold_spmspv(torch, celty, enc, p, None, args.steps, args.warmup)
+            err = ref.rel_error(sp_["y"].astype(np.float64), ref.spmspv_dense_fp64(p.W, p.mask, p.x, p.tau))
+            d = cold_dense(torch, F, p, args.steps)
+            speed.setdefault(pct, []).append(d["us"] / sp_["us"])
+            print(json.dumps({"M": M, "K": K, "dual_sparsity_pct": pct, "R": R, "launch": plan,
+                              "us": round(sp_["us"], 3), "alg_GBps": round(b_alg / sp_["us"] / 1e3, 1),
+                              "pct_peak_alg": round(100 * b_alg / sp_["us"] / 1e3 / PEAK_HBM_GBPS, 2),
+                              "pct_peak_fetched": round(100 * comp / sp_["us"] / 1e3 / PEAK_HBM_GBPS, 2),
+                              "dense_us": d["us"], "speedup_vs_dense": round(d["us"] / sp_["us"], 3),
+                              "rel_err": float(f"{err:.3e}")}), flush=True)
+            assert err <= 2e-3, err
+    print(json.dumps({"paper_shapes_mean_speedup_vs_dense": {str(k): round(float(np.mean(v)), 3)
+                                                             for k, v in speed.items()},
+                      "paper_shapes_max_speedup_vs_dense": {str(k): round(float(np.max(v)), 3)
+                                                            for k, v in speed.items()},
+                      "shapes": [f"{M}x{K}" for M, K in PAPER_SHAPES], "data": "synthetic"}))
+    return 0
 
 
 def cpu_baseline(p, budget_s: float) -> dict:
@@ -400,6 +510,8 @@ def main() -> int:
     ap.add_argument("--seq-as", type=float, default=None, help="activation sparsity of --sequence")
     ap.add_argument("--format-study", action="store_true",
                     help="host only: RLC-CSC vs bitmap vs dense sizes across weight sparsity")
+    ap.add_argument("--paper-shapes", action="store_true",
+                    help="the paper's six kernel shapes at 30/50/70%% dual sparsity vs dense GEMV")
     ap.add_argument("--encode-throughput", action="store_true",
                     help="host only: encoder throughput on the benchmark matrices")
     args = ap.parse_args()
@@ -417,6 +529,8 @@ def main() -> int:
 
     if args.sequence:
         return sequence_bench(args)
+    if args.paper_shapes:
+        return paper_shapes(args)
 
     import torch
     import torch.nn.functional as F
@@ -443,27 +557,10 @@ def main() -> int:
         return record_traffic(workload_key, args.record_traffic, cmds)
     dev = torch.device("cuda:0")
     b_alg, e_a, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
-    sbytes = stored_bytes(enc)
-    ncopies = 1 if args.hot else max(2, -(-COLD_BYTES // sbytes))
-    base = enc.to_device(dev)
-    copies = [base] + [base.clone_to() for _ in range(ncopies - 1)]
-    x = torch.from_numpy(p.x.view(np.int16)).to(dev)
-    y = torch.empty(M, dtype=torch.int16, device=dev)
-    ws = celty.new_workspace(base, dev)
-    def step(i):
-        # stream = None: the binding launches on torch's current stream, which
-        # is the capture stream while a graph is being recorded
-        celty.celty_spmspv_ex(copies[i % ncopies], x, p.tau, y, ws, launch)
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    print(f"[bench] warmup done: {M}x{K} ws{args.ws:g} as{args.as_:g} R={R} copies={ncopies} plan={plan}",
-          file=sys.stderr, flush=True)
-    eager_us = time_loop(torch, step, args.steps)
-    # the timed region: K steps captured in one HIP graph and replayed on the
-    # launch stream; one step is exactly one kernel launch
-    us_step, samples = time_graph(torch, lambda i: step(i), args.steps)
+    comp_fetched, total_fetched = fetched_bytes_from_encoding(enc, g_a, plan)
+    print(f"[bench] {M}x{K} ws{args.ws:g} as{args.as_:g} R={R} plan={plan}", file=sys.stderr, flush=True)
+    run = cold_spmspv(torch, celty, enc, p, launch, args.steps, args.warmup, args.hot)
+    us_step, samples, eager_us, ncopies = run["us"], run["samples"], run["eager_us"], run["copies"]
     us_kernel = us_step
     print(f"[bench] timed: {us_step:.3f} us/step (graph), eager {eager_us:.2f} us/call", file=sys.stderr, flush=True)
 
@@ -472,24 +569,7 @@ def main() -> int:
     floor_wall = time_loop(torch, lambda i: tiny.fill_(1.0), args.steps)
     floor_kernel, _ = time_graph(torch, lambda i: tiny.fill_(1.0), args.steps)
 
-    dense = None
-    if not args.no_dense:
-        Wf = torch.from_numpy(np.where(p.mask != 0, p.W, np.float16(0))).to(dev)
-        nd = 1 if args.hot else max(2, -(-COLD_BYTES // (2 * M * K)))
-        dcopies = [Wf] + [Wf.clone() for _ in range(nd - 1)]
-        xd = torch.from_numpy(np.where(np.abs(p.x.astype(np.float32)) > p.tau, p.x, np.float16(0))).to(dev)[None]
-        for i in range(20):
-            F.linear(xd, dcopies[i % nd])
-        try:
-            dense_us, _ = time_graph(torch, lambda i: F.linear(xd, dcopies[i % nd]), args.steps)
-            dense_mode = "graph"
-        except Exception:
-            dense_us, dense_mode = time_loop(torch, lambda i: F.linear(xd, dcopies[i % nd]), args.steps), "eager"
-        dense = {"us": round(dense_us, 3), "GBps": round((2 * M * K + 2 * K + 2 * M) / dense_us / 1e3, 1),
-                 "op": "torch.nn.functional.linear fp16, batch 1 (hipBLASLt/rocBLAS)", "copies": nd,
-                 "timing": dense_mode}
-        del dcopies, Wf
-        torch.cuda.empty_cache()
+    dense = None if args.no_dense else cold_dense(torch, F, p, args.steps, args.hot)
 
     cpu = None
     if not args.no_cpu:
@@ -521,6 +601,9 @@ def main() -> int:
         "pct_peak_hbm": round(100 * gbps_step / PEAK_HBM_GBPS, 2),
         "algorithmic_bytes": b_alg,
         "active_entries": e_a,
+        "compressed_bytes_fetched": comp_fetched,
+        "pct_peak_hbm_fetched": round(100 * comp_fetched / us_step / 1e3 / PEAK_HBM_GBPS, 2),
+        "bytes_requested": total_fetched,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
                      "kernel_us": round(us_kernel, 3), "kernel_us_replays": [round(v, 3) for v in samples],
