@@ -7,8 +7,9 @@
 * edge shapes: M < R, M % R != 0, K = 1, K not a multiple of 64, R = 1;
 * every launch shape gives the same answer within tolerance;
 * the workspace is left zero-filled by every call; y is fully overwritten;
-* full-size runs of all five benchmark configurations in the launch shape
-  the benchmark uses.
+* full-size runs of all five benchmark configurations, and of the paper's
+  kernel shapes at 30/50/70 % dual sparsity, in the launch shape the
+  benchmark uses.
 """
 import numpy as np
 import pytest
@@ -246,6 +247,15 @@ def test_config5_projections(celty, torch_dev, as_):
         p = workloads.make_problem(5, proj.M, proj.K, c["ws"], as_, c["xdist"], seed=0, layer=0,
                                    proj=workloads.PROJ_IDS[name], x=x)
         _full(celty, torch_dev, p, f"config5 as{as_} {name}")
+
+
+@pytest.mark.parametrize("pct", [30, 50, 70])
+@pytest.mark.parametrize("M,K", [(4096, 11008), (5120, 5120), (5120, 13824), (7168, 7168), (7168, 28672)])
+def test_paper_kernel_shapes(celty, torch_dev, M, K, pct):
+    # the paper's kernel workloads (Section 5) at weight = activation sparsity,
+    # the problems bench.py --paper-shapes times (4096^2 is config 2 above)
+    p = workloads.make_problem(2, M, K, pct, pct, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
+    _full(celty, torch_dev, p, f"paper shape {M}x{K} dual{pct}")
 
 
 # --------------------------------------------------------------------------
