@@ -129,12 +129,16 @@ celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* ma
 /*
  * Active-column selection (Sections 1, 2.1 and 3.1: magnitude threshold,
  * then stream compaction by wavefront ballot and prefix sums).
- *   x      device, fp16[K].
+ *   x      device, fp16[K], 2-byte aligned (4-byte alignment lets the kernel
+ *          read two columns per 32-bit load; the result is the same).
  *   tau    threshold; column k is active iff |x_k| > tau in fp32 (NaN x_k is
  *          never active; tau < 0 makes every non-NaN column active).
- *   idx    device, int32[K]: receives the active indices in ascending order.
+ *   idx    device, int32[K]: receives the active indices in ascending order;
+ *          entries past |A| are not written.
  *   count  device, int32[1]: receives |A|.
- * Errors: EINVAL (null pointers, K < 1, NaN tau, misaligned idx/count), EHIP.
+ * One kernel launch of one workgroup.
+ * Errors: EINVAL (null pointers, K < 1 or K > (2^31 - 4) / 2, NaN tau,
+ * misaligned x/idx/count), EHIP.
  */
 celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int32_t* count,
                           void* stream);

@@ -11,7 +11,8 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libcelty.so")
-SOURCES = [os.path.join(PKG, "csrc", "spmspv.hip"), os.path.join(PKG, "csrc", "encode.cpp")]
+SOURCES = [os.path.join(PKG, "csrc", "spmspv.hip"), os.path.join(PKG, "csrc", "select.hip"),
+           os.path.join(PKG, "csrc", "encode.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -38,10 +38,10 @@
 #include <cstdint>
 
 #include "celty.h"
+#include "common.h"
 
 namespace {
 
-constexpr int kWave = 64;
 constexpr int kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kSlack = 8 + 128;       // tile rows past R: alignment entries, and the cap's reach
 constexpr int kMaxSlices = 63;        // column slices per row tile (merge ticket count byte)
@@ -54,24 +54,8 @@ struct SegInfo {
   float xs;          // x_k * 2^s (s: the workgroup's fixed-point scale)
 };
 
-__device__ __forceinline__ float half_bits_to_float(uint32_t bits) {
-  return __half2float(__ushort_as_half(static_cast<unsigned short>(bits)));
-}
-
 __device__ __forceinline__ unsigned short float_to_half_bits(float v) {
   return __half_as_ushort(__float2half_rn(v));
-}
-
-// DPP row shifts inside each 16-lane row, then row broadcasts of lanes 15
-// and 31: inclusive scan over the 64 lanes.
-__device__ __forceinline__ int wave_inclusive_scan(int v) {
-  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);   // row_shr:1
-  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);   // row_shr:2
-  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);   // row_shr:4
-  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);   // row_shr:8
-  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);   // row_bcast:15 -> rows 1, 3
-  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);   // row_bcast:31 -> rows 2, 3
-  return v;
 }
 
 // The same pattern with max: lane 63 ends with the wavefront maximum.
@@ -91,11 +75,6 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
-  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
 // Inclusive scan / suffix minimum over the 16 lanes of each DPP row.
@@ -652,36 +631,6 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs b
   spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.K, p.Kc, p.KC, p.tau}, p, static_cast<int>(blockIdx.x));
 }
 
-// Global selection: one workgroup of 1024 lanes walks x in 1024-wide steps;
-// ballot + mbcnt give each active lane its rank, wave totals are combined in
-// LDS, and indices are written in ascending order.
-__global__ __launch_bounds__(1024) void select_kernel(const unsigned short* __restrict__ x, int K, float tau,
-                                                      int32_t* __restrict__ idx, int32_t* __restrict__ count) {
-  constexpr int NW = 1024 / kWave;
-  __shared__ uint32_t wsum[NW];
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  uint32_t base = 0;
-  for (int it = 0; it < K; it += 1024) {
-    const int k = it + tid;
-    const bool act = k < K && fabsf(half_bits_to_float(x[k])) > tau;
-    const uint64_t m = __ballot(act);
-    const uint32_t rank = lanes_below(m);
-    if (lane == 0) wsum[wv] = static_cast<uint32_t>(__popcll(m));
-    __syncthreads();
-    uint32_t off = base, tot = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const uint32_t cw = wsum[w];
-      if (w < wv) off += cw;
-      tot += cw;
-    }
-    if (act) idx[off + rank] = k;
-    base += tot;
-    __syncthreads();
-  }
-  if (tid == 0) *count = static_cast<int32_t>(base);
-}
-
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
@@ -693,8 +642,6 @@ struct Plan {
   int64_t blocks = 0;
   size_t lds = 0;
 };
-
-bool misaligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
 
 celty_status check_header(const celty_rlc_csc* W) {
   if (!W) return CELTY_EINVAL;
@@ -964,15 +911,6 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
 extern "C" celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y, void* workspace,
                                      size_t workspace_bytes, void* stream) {
   return celty_spmspv_ex(W, x, tau, y, workspace, workspace_bytes, nullptr, stream);
-}
-
-extern "C" celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int32_t* count,
-                                     void* stream) {
-  if (!x || !idx || !count || K < 1 || std::isnan(tau)) return CELTY_EINVAL;
-  if (misaligned(x, 2) || misaligned(idx, 4) || misaligned(count, 4)) return CELTY_EINVAL;
-  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(1024), 0, static_cast<hipStream_t>(stream),
-                     static_cast<const unsigned short*>(x), K, tau, idx, count);
-  return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
 }
 
 extern "C" const char* celty_status_string(celty_status status) {

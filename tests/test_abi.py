@@ -303,6 +303,8 @@ def test_select_rejects_bad_arguments():
     assert f(FAKE, 0, 0.5, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
     assert f(FAKE, 10, math.nan, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
     assert f(FAKE, 10, 0.5, FAKE + 66, FAKE + 128, None) == CELTY_EINVAL
+    # x's byte size must fit the kernel's 32-bit buffer size
+    assert f(FAKE, 2**30, 0.5, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
 
 
 def test_single_hip_runtime_alongside_torch():

@@ -69,7 +69,8 @@ def _check(y, W, mask, x, tau):
 # --------------------------------------------------------------------------
 # selection
 # --------------------------------------------------------------------------
-@pytest.mark.parametrize("K", [1, 63, 64, 65, 1000, 1024, 1025, 4096, 11008, 28672])
+@pytest.mark.parametrize("K", [1, 63, 64, 65, 1000, 1024, 1025, 4096, 11008, 28672, 32767, 32768, 32769,
+                               65600, 100000])
 @pytest.mark.parametrize("mode", ["median", "neg", "zero", "max", "nan"])
 def test_select_bit_exact(celty, torch_dev, K, mode):
     torch, dev = torch_dev
@@ -89,7 +90,31 @@ def test_select_bit_exact(celty, torch_dev, K, mode):
     want = ref.select_active(x, tau)
     n = int(cnt.item())
     assert n == want.size
-    assert np.array_equal(idx[:n].cpu().numpy(), want)
+    got = idx.cpu().numpy()
+    assert np.array_equal(got[:n], want)
+    assert np.all(got[n:] == -7), "selection wrote past the active count"
+
+
+@pytest.mark.parametrize("K", [1, 2, 1025, 28672, 32769])
+def test_select_x_only_two_byte_aligned(celty, torch_dev, K):
+    # x one element into a buffer: 2-byte but not 4-byte aligned (the path
+    # without word loads)
+    torch, dev = torch_dev
+    _note(f"select misaligned K={K}")
+    rng = np.random.default_rng(K + 7)
+    x = rng.laplace(size=K + 1).astype(np.float16)
+    tau = workloads.tau_for_sparsity(x[1:], 50)
+    buf = torch.from_numpy(x.view(np.int16)).to(dev)
+    xt = buf[1:]
+    assert xt.data_ptr() % 4 == 2
+    idx = torch.full((K,), -7, dtype=torch.int32, device=dev)
+    cnt = torch.zeros(1, dtype=torch.int32, device=dev)
+    celty.celty_select(xt, tau, idx, cnt)
+    torch.cuda.synchronize()
+    want = ref.select_active(x[1:], tau)
+    n = int(cnt.item())
+    got = idx.cpu().numpy()
+    assert n == want.size and np.array_equal(got[:n], want) and np.all(got[n:] == -7)
 
 
 # --------------------------------------------------------------------------
