@@ -590,6 +590,8 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "arithmetic": "fp16 W and x; every product exact in fp32; sums in int32 fixed point per workgroup "
+                      "and int64 across column slices (at least as accurate as fp32 accumulation); y fp16 (RNE)",
         "data": "synthetic",
         "config": {"workload": workload, "workload_key": workload_key, "M": M, "K": K, "weight_sparsity_pct": args.ws,
                    "activation_sparsity_pct": args.as_, "tile_rows_R": R, "storage": "fp16 values + 4-bit runs",
