@@ -496,6 +496,9 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--sigma", type=float, default=0.0,
+                    help="outlier input features: per-feature scales exp(sigma*N(0,1)) on W's columns and x, "
+                         "per-row magnitude pruning (0 = the uniform-mask workload)")
     ap.add_argument("--hot", action="store_true", help="reuse one copy (cache-resident; diagnostic)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of a known size (counter calibration)")
@@ -536,16 +539,20 @@ def main() -> int:
     import workloads
 
     M, K = args.M, args.K
-    headline = (M, K, args.ws, args.as_) == (4096, 4096, 70.0, 70.0)
-    p = workloads.make_problem(2, M, K, args.ws, args.as_, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
+    headline = (M, K, args.ws, args.as_) == (4096, 4096, 70.0, 70.0) and not args.sigma
+    if args.sigma:
+        p = workloads.outlier_feature_problem(M, K, int(args.ws), args.as_, args.sigma)
+    else:
+        p = workloads.make_problem(2, M, K, args.ws, args.as_, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
     R = args.R or celty.default_tile_rows(M, K)
     enc = celty.celty_encode(p.W, p.mask, R)
     launch = (args.cols, args.waves) if (args.cols or args.waves) else None
     plan = celty.celty_spmspv_plan(enc, launch)
-    workload_key = (f"{M}x{K}-ws{args.ws:g}-as{args.as_:g}-R{R}-"
+    workload_key = (f"{M}x{K}-ws{args.ws:g}-as{args.as_:g}" + (f"-sigma{args.sigma:g}" if args.sigma else "") + f"-R{R}-"
                     f"{plan['cols_per_block']}x{plan['waves_per_block']}x{plan['groups_per_lane']}")
     if args.record_traffic:
         flags = f" --M {M} --K {K} --ws {args.ws:g} --as {args.as_:g}" + (f" --R {args.R}" if args.R else "") + \
+                (f" --sigma {args.sigma:g}" if args.sigma else "") + \
                 (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "")
         cmds = [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py "
                 f"--steps 200 --warmup 20 --no-cpu --no-dense{flags}" for c in ("FETCH_SIZE", "WRITE_SIZE")]
@@ -578,6 +585,9 @@ def main() -> int:
     traffic = None if args.hot else measured_traffic(workload_key)
     workload = (f"{M}x{K} fp16 W (out x in), {args.ws:g}% unstructured weight sparsity + "
                 f"{args.as_:g}% activation sparsity (Laplace x, magnitude threshold), batch 1")
+    if args.sigma:
+        workload += (f"; outlier input features (per-feature scale exp({args.sigma:g}*N(0,1)) on W's columns "
+                     f"and x, per-row magnitude pruning)")
     out = {
         "metric": METRIC if headline else f"us/SpMSpV + effective HBM GB/s, {M}x{K} at ws{args.ws:g}/as{args.as_:g}",
         "value": round(us_step, 3),

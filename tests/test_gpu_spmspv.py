@@ -283,6 +283,15 @@ def test_paper_kernel_shapes(celty, torch_dev, M, K, pct):
     _full(celty, torch_dev, p, f"paper shape {M}x{K} dual{pct}")
 
 
+@pytest.mark.parametrize("M,K,sigma", [(4096, 4096, 1.0), (4096, 11008, 1.0), (11008, 4096, 2.0),
+                                         (28672, 8192, 1.0)])
+def test_outlier_features(celty, torch_dev, M, K, sigma):
+    # per-feature scales shared by W's columns and x: column densities from ~0
+    # to ~95 %, magnitudes over several decades inside one column slice
+    p = workloads.outlier_feature_problem(M, K, 50, 50, sigma)
+    _full(celty, torch_dev, p, f"outlier features {M}x{K} sigma{sigma}")
+
+
 # --------------------------------------------------------------------------
 # several products in one launch
 # --------------------------------------------------------------------------

@@ -160,6 +160,29 @@ def make_problem(config: int, M: int, K: int, ws: float, as_: float, xdist: str,
     return Problem(W=W, mask=mask, x=x, tau=tau, meta=meta)
 
 
+def outlier_feature_problem(M: int, K: int, ws: int, as_: float, sigma: float = 1.0,
+                            seed: int = 0) -> Problem:
+    """A layer with outlier input features: every input feature k gets a scale
+    c_k = exp(sigma * N(0, 1)) shared by column k of W and by x_k, so large-scale
+    columns keep more weights under per-row magnitude pruning and are also the
+    ones whose activations pass the threshold (column densities from about 0
+    to 95 % at sigma = 1).  Draw order: c, then W (N(0, 0.02) * c_k), then x
+    (Laplace(0, 1) * c_k); mask by per-row magnitude; tau as for make_problem.
+    Generator id: config 6."""
+    rng = rng_for(6, seed, 0, PROJ_IDS["w"])
+    c = np.exp(sigma * rng.standard_normal(K)).astype(np.float32)
+    w = rng.standard_normal((M, K), dtype=np.float32)
+    w *= np.float32(0.02)
+    w *= c[None, :]
+    W = w.astype(np.float16)
+    mask = mask_row_magnitude(W, int(ws))
+    x = (rng.laplace(0.0, 1.0, K) * c).astype(np.float16)
+    tau = tau_for_sparsity(x, as_)
+    meta = dict(config=6, M=M, K=K, ws=ws, as_=as_, xdist="laplace*c", sigma=sigma, seed=seed,
+                mask="row_magnitude")
+    return Problem(W=W, mask=mask, x=x, tau=tau, meta=meta)
+
+
 def shared_x(config: int, seed: int, layer: int, group: str, K: int, xdist: str) -> np.ndarray:
     """The activation vector shared by projections of one x-group in a layer."""
     gid = {"attn_in": 100, "attn_out": 101, "mlp_in": 102, "mlp_mid": 103}[group]
