@@ -423,6 +423,36 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int t = blk / e.KC, c = blk - t * e.KC;
+
+  // The selection's loads go first: they need only the leading (preloaded)
+  // arguments, so the workgroup's first memory round trip does not wait for
+  // the rest of its argument block or for the LDS initialisation.
+  const int k0 = c * e.Kc;
+  const int kn = min(e.Kc, e.K - k0);
+  const uint32_t* gp = e.gptr + static_cast<size_t>(t) * e.K + k0;
+  const bool one_per_lane = kn <= NT;   // workgroup-uniform
+  uint32_t g[kMaxCols + 1], xr[kMaxCols];
+  int m = 1, kb = tid;
+  if (one_per_lane) {
+    g[0] = g[1] = xr[0] = 0u;
+    if (tid < kn) {
+      g[0] = gp[tid];
+      g[1] = gp[tid + 1];
+      xr[0] = e.x[k0 + tid];
+    }
+  } else {
+    // m <= kMaxCols consecutive columns per lane; all kMaxCols slots are
+    // loaded, at clamped indices and without branches, so that no load waits
+    // for another (columns at or past kn, or past the lane's m, are dropped
+    // by the keep test)
+    m = (kn + NT - 1) / NT;
+    kb = tid * m;
+#pragma unroll
+    for (int j = 0; j <= kMaxCols; ++j) g[j] = gp[min(kb + j, kn)];
+#pragma unroll
+    for (int j = 0; j < kMaxCols; ++j) xr[j] = e.x[k0 + min(kb + j, kn - 1)];
+  }
+
   const int row0 = t * p.R;
   const int rows = min(p.R, p.M - row0);
   const int base4_cap = 4 * (p.R + 7);   // tile byte address cap of a group base
@@ -436,19 +466,11 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // The flat group sequence is then cut into one range per wavefront:
   // segment i goes to wavefront wave_of(off_i), and wfirst[w] collects the
   // lowest segment index of wavefront w (INT_MAX when none starts there).
-  const int k0 = c * e.Kc;
-  const int kn = min(e.Kc, e.K - k0);
-  const uint32_t* gp = e.gptr + static_cast<size_t>(t) * e.K + k0;
   uint32_t n_seg, n_grp;
-  if (kn <= NT) {
+  if (one_per_lane) {
     // one column per lane
-    uint32_t g0 = 0u, g1 = 0u, xr = 0u;
-    if (tid < kn) {
-      g0 = gp[tid];
-      g1 = gp[tid + 1];
-      xr = e.x[k0 + tid];
-    }
-    const float xv = half_bits_to_float(xr);
+    const uint32_t g0 = g[0], g1 = g[1];
+    const float xv = half_bits_to_float(xr[0]);
     const bool keep = tid < kn && fabsf(xv) > e.tau && g1 > g0;
     const uint32_t cnt = keep ? g1 - g0 : 0u;
     // |x| >= 0 orders like its bit pattern
@@ -463,18 +485,8 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     }
     scale = s;
   } else {
-    // m <= kMaxCols consecutive columns per lane, so one block scan still
-    // orders all of them: segment order is column order
-    const int m = (kn + NT - 1) / NT;
-    const int kb = tid * m;
-    // all kMaxCols slots are loaded, at clamped indices and without branches,
-    // so that no load waits for another; columns at or past kn, or past the
-    // lane's m, are dropped by the keep test
-    uint32_t g[kMaxCols + 1], xr[kMaxCols];
-#pragma unroll
-    for (int j = 0; j <= kMaxCols; ++j) g[j] = gp[min(kb + j, kn)];
-#pragma unroll
-    for (int j = 0; j < kMaxCols; ++j) xr[j] = e.x[k0 + min(kb + j, kn - 1)];
+    // m <= kMaxCols consecutive columns per lane (loaded above), so one block
+    // scan still orders all of them: segment order is column order
     uint32_t keep_bits = 0u, n_loc = 0u, g_loc = 0u, m_loc = 0u;
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) {
