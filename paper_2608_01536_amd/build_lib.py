@@ -19,9 +19,10 @@ FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",
     # packed fp32 VALU forms stay off (the compiler must not emit v_pk_*_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # the leading kernel arguments (those a workgroup's first loads need) are
-    # preloaded into scalar registers at dispatch instead of fetched from memory
-    "-Xarch_device", "-mllvm=-amdgpu-kernarg-preload-count=6",
+    # the leading kernel arguments (those a workgroup's prologue needs: the
+    # selection's pointers and sizes, the LDS layout, max|w|, R and M; 14
+    # scalar registers) are preloaded at dispatch instead of fetched from memory
+    "-Xarch_device", "-mllvm=-amdgpu-kernarg-preload-count=13",
     "-I", os.path.join(ROOT, "include"), "-pthread",
 ]
 

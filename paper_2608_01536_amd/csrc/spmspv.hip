@@ -395,16 +395,20 @@ struct BatchArgs {
   KernelArgs prod[kMaxBatch];
 };
 
-// The arguments the first loads of a workgroup need.  A single-product
-// launch passes them as leading kernel arguments, which gfx950 preloads into
-// scalar registers at dispatch (the library is built with
-// -amdgpu-kernarg-preload-count), so a workgroup's first memory round trip
-// does not wait for its argument block to be fetched.
+// The arguments a workgroup's prologue needs (the selection's pointers and
+// sizes, the LDS layout, max|w|, R and M).  A single-product launch passes
+// them as leading kernel arguments, which gfx950 preloads into scalar
+// registers at dispatch (the library is built with
+// -amdgpu-kernarg-preload-count), so neither the selection's first memory
+// round trip nor the LDS initialisation waits for the argument block.
 struct Early {
   const uint32_t* gptr;
   const unsigned short* x;
   int K, Kc, KC;
   float tau;
+  int tile_slots, seg_off, scr_off, misc_off;   // LDS layout
+  float max_abs;
+  int R, M;
 };
 
 // One workgroup's share of product p: row tile and column slice number blk.
@@ -416,9 +420,9 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // the tile's LDS byte address (for the accumulation's own LDS instructions)
   const uint32_t tile_lds = static_cast<uint32_t>(
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem));
-  SegInfo* seg = reinterpret_cast<SegInfo*>(smem + p.seg_off);
-  int* scr_all = reinterpret_cast<int*>(smem + p.scr_off);
-  uint32_t* part = reinterpret_cast<uint32_t*>(smem + p.misc_off);   // 3*WAVES
+  SegInfo* seg = reinterpret_cast<SegInfo*>(smem + e.seg_off);
+  int* scr_all = reinterpret_cast<int*>(smem + e.scr_off);
+  uint32_t* part = reinterpret_cast<uint32_t*>(smem + e.misc_off);   // 3*WAVES
   int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
@@ -453,11 +457,11 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     for (int j = 0; j < kMaxCols; ++j) xr[j] = e.x[k0 + min(kb + j, kn - 1)];
   }
 
-  const int row0 = t * p.R;
-  const int rows = min(p.R, p.M - row0);
-  const int base4_cap = 4 * (p.R + 7);   // tile byte address cap of a group base
+  const int row0 = t * e.R;
+  const int rows = min(e.R, e.M - row0);
+  const int base4_cap = 4 * (e.R + 7);   // tile byte address cap of a group base
 
-  for (int i = tid; i < p.tile_slots; i += NT) tile[i] = 0;
+  for (int i = tid; i < e.tile_slots; i += NT) tile[i] = 0;
   for (int i = tid; i < NT * G; i += NT) scr_all[i] = 0;
   if (tid < WAVES) wfirst[tid] = INT_MAX;
   int scale = 0;   // the workgroup's fixed-point scale 2^scale
@@ -477,7 +481,7 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     uint32_t en, eg, xmax_bits;
     block_scan_select<WAVES>(keep ? 1u : 0u, cnt, keep ? __float_as_uint(fabsf(xv)) : 0u, en, eg, n_seg, n_grp,
                              xmax_bits, part);
-    const int s = fixed_point_scale(n_seg, p.max_abs, xmax_bits);
+    const int s = fixed_point_scale(n_seg, e.max_abs, xmax_bits);
     const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
     if (keep) {
       seg[en] = SegInfo{g0, eg, cnt, ldexpf(xv, s)};
@@ -499,7 +503,7 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     }
     uint32_t en, eg, xmax_bits;
     block_scan_select<WAVES>(n_loc, g_loc, m_loc, en, eg, n_seg, n_grp, xmax_bits, part);
-    const int s = fixed_point_scale(n_seg, p.max_abs, xmax_bits);
+    const int s = fixed_point_scale(n_seg, e.max_abs, xmax_bits);
     const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
     uint32_t idx = en, off = eg;
 #pragma unroll
@@ -631,8 +635,11 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
 
 template <int WAVES, int G, int DEPTH>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(const uint32_t* gptr, const unsigned short* x, int K,
-                                                                int Kc, int KC, float tau, KernelArgs p) {
-  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, K, Kc, KC, tau}, p, static_cast<int>(blockIdx.x));
+                                                                int Kc, int KC, float tau, int tile_slots, int seg_off,
+                                                                int scr_off, int misc_off, float max_abs, int R, int M,
+                                                                KernelArgs p) {
+  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, K, Kc, KC, tau, tile_slots, seg_off, scr_off, misc_off, max_abs, R, M}, p,
+                                static_cast<int>(blockIdx.x));
 }
 
 template <int WAVES, int G, int DEPTH>
@@ -640,7 +647,9 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs b
   const int pi = static_cast<int>(blockIdx.y);
   if (static_cast<int>(blockIdx.x) >= ba.blocks[pi]) return;   // past this product's grid
   const KernelArgs& p = ba.prod[pi];
-  spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.K, p.Kc, p.KC, p.tau}, p, static_cast<int>(blockIdx.x));
+  spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.K, p.Kc, p.KC, p.tau, p.tile_slots, p.seg_off, p.scr_off,
+                                      p.misc_off, p.max_abs, p.R, p.M},
+                                p, static_cast<int>(blockIdx.x));
 }
 
 // ---------------------------------------------------------------------------
@@ -746,7 +755,8 @@ celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stre
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_kernel<WAVES, G, DEPTH>, single_attr)) return CELTY_EHIP;
     const KernelArgs& q = a.prod[0];
     hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.max_blocks)),
-                       dim3(WAVES * kWave), ln.lds, stream, q.gptr, q.x, q.K, q.Kc, q.KC, q.tau, q);
+                       dim3(WAVES * kWave), ln.lds, stream, q.gptr, q.x, q.K, q.Kc, q.KC, q.tau, q.tile_slots,
+                       q.seg_off, q.scr_off, q.misc_off, q.max_abs, q.R, q.M, q);
   } else {
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_batch_kernel<WAVES, G, DEPTH>, batch_attr))
       return CELTY_EHIP;
