@@ -607,9 +607,9 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     return;
   }
   // Taller tiles: a lane's rows go J at a time (J = 2 up to twice the
-  // workgroup's lanes, else 4), their atomics issued back to back (a row past
-  // the tile adds a zero ticket to slot 0 of the tile, which changes nothing,
-  // so no branch separates them), then their returns are examined.
+  // workgroup's lanes, else 4), their atomics issued back to back under the
+  // execution mask (rows past a partial last tile issue none), then their
+  // returns are examined.
   const auto merge_rows = [&](auto in_flight) {
     constexpr int J = decltype(in_flight)::value;
     for (int r0 = tid; r0 < rows; r0 += J * NT) {
@@ -617,10 +617,14 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         const int r = r0 + j * NT;
-        const bool in = r < rows;
-        ticket[j] = in ? kCount + static_cast<unsigned long long>(fixed_at_launch_scale(tile[in ? r : 0]) + kBias)
-                       : 0ull;
-        old[j] = atomicAdd(p.ws + row0 + (in ? r : 0), ticket[j]);
+        ticket[j] = 0ull;
+        old[j] = 0ull;
+        // rows past the tile take no atomic: a shared dummy slot would
+        // serialise every such lane of every slice on one address
+        if (r < rows) {
+          ticket[j] = kCount + static_cast<unsigned long long>(fixed_at_launch_scale(tile[r]) + kBias);
+          old[j] = atomicAdd(p.ws + row0 + r, ticket[j]);
+        }
       }
 #pragma unroll
       for (int j = 0; j < J; ++j)

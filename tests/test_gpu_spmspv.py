@@ -283,6 +283,21 @@ def test_paper_kernel_shapes(celty, torch_dev, M, K, pct):
     _full(celty, torch_dev, p, f"paper shape {M}x{K} dual{pct}")
 
 
+@pytest.mark.parametrize("M,R,launch", [
+    (22016, 2048, None),             # last tile 1536 rows: two rows per lane, the second past the tile for half
+    (2 * 4096 + 3000, 4096, (256, 16, 1)),   # last tile 3000 rows: four rows per lane
+    (5 * 2048 + 1025, 2048, (128, 16, 2)),
+    (3 * 1024 + 700, 1024, (128, 8, 1)),
+])
+def test_partial_last_tile_taller_than_the_workgroup(celty, torch_dev, M, R, launch):
+    # the merge takes several rows per lane; rows past a partial last tile must
+    # neither change y nor leave the workspace dirty
+    p = workloads.make_problem(2, M, 4096, 50, 50, "laplace", seed=3, proj=workloads.PROJ_IDS["w"])
+    _note(f"partial tile M={M} R={R} launch={launch}")
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, R, launch=launch)
+    _check(y, p.W, p.mask, p.x, p.tau)
+
+
 @pytest.mark.parametrize("M,K,sigma", [(4096, 4096, 1.0), (4096, 11008, 1.0), (11008, 4096, 2.0),
                                          (28672, 8192, 1.0)])
 def test_outlier_features(celty, torch_dev, M, K, sigma):
