@@ -298,6 +298,25 @@ def test_partial_last_tile_taller_than_the_workgroup(celty, torch_dev, M, R, lau
     _check(y, p.W, p.mask, p.x, p.tau)
 
 
+@pytest.mark.parametrize("config,group", [(3, ("q", "k", "v")), (3, ("gate", "up")), (5, ("q", "k", "v"))])
+def test_stacked_projections(celty, torch_dev, config, group):
+    # projections reading one x stacked into one taller matrix at encode time
+    # (the fused decode-step schedule): each block of y matches its own oracle
+    probs = {p.meta["proj_name"]: p for p in workloads.layer_problems(config, 0, 0, as_=60 if config == 5 else None)}
+    ps = [probs[n] for n in group]
+    W = np.concatenate([p.W for p in ps])
+    mask = np.concatenate([p.mask for p in ps])
+    from paper_2608_01536_amd import default_tile_rows
+    R = default_tile_rows(*W.shape)
+    _note(f"stacked config{config} {group} {W.shape} R={R}")
+    y = _run(celty, torch_dev, W, mask, ps[0].x, ps[0].tau, R)
+    r0 = 0
+    for p in ps:
+        m = p.W.shape[0]
+        _check(y[r0:r0 + m], p.W, p.mask, p.x, p.tau)
+        r0 += m
+
+
 @pytest.mark.parametrize("M,K,sigma", [(4096, 4096, 1.0), (4096, 11008, 1.0), (11008, 4096, 2.0),
                                          (28672, 8192, 1.0)])
 def test_outlier_features(celty, torch_dev, M, K, sigma):
