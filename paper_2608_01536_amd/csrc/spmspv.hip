@@ -46,6 +46,9 @@ constexpr int kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kSlack = 8 + 128;       // tile rows past R: alignment entries, and the cap's reach
 constexpr int kMaxSlices = 63;        // column slices per row tile (merge ticket count byte)
 constexpr int kMaxCols = 8;           // columns per thread in the selection
+// Cache policy of the value loads: non-temporal (the nt bit of gfx950's
+// buffer loads), so the streamed weights do not displace cached lines.
+constexpr int kStreamPolicy = 2;
 
 struct SegInfo {
   uint32_t gstart;   // first group of the segment in the values/runs arrays
@@ -262,10 +265,12 @@ __device__ __forceinline__ void fetch_pass(Pass<G>& a, const Streams& st, const 
   }
   // Loads are issued by every lane of every pass (idle lanes and idle passes
   // read group 0 and drop it), so the wait for one pass's data can leave the
-  // later passes' loads in flight.
+  // later passes' loads in flight.  The values are streamed non-temporally
+  // (each of their lines is read once); the runs keep the default policy,
+  // since a pass's 256 bytes of runs usually share a line with the next pass.
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(st.values, static_cast<int>(gl[i] << 4), 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(st.values, static_cast<int>(gl[i] << 4), 0, kStreamPolicy);
     a.v[i] = make_uint4(v[0], v[1], v[2], v[3]);
     a.rw[i] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>(gl[i] << 2), 0, 0);
   }
