@@ -157,9 +157,10 @@ typedef struct celty_launch {
 } celty_launch;
 
 /* A tile height R for encoding an M x K matrix for celty_spmspv (host only):
- * the largest power of two at or below M / 8, clamped to [256, 2048], which
- * gives 8 to 16 row tiles for the LLM projection shapes and keeps one tile's
- * accumulator (4 * (R + 136) bytes of LDS) small.  0 when M < 1. */
+ * the largest power of two at or below M / 8 (M / 4 when K >= 4 M), clamped
+ * to [256, 2048], which gives 4 to 16 row tiles for the LLM projection shapes
+ * and keeps one tile's accumulator (4 * (R + 136) bytes of LDS) small.
+ * 0 when M < 1. */
 int32_t celty_default_tile_rows(int32_t M, int32_t K);
 
 /* Bytes of device workspace celty_spmspv needs for this shape: one 64-bit

@@ -841,10 +841,13 @@ celty_status product_args(const celty_rlc_csc* W, const Plan& pl, const void* x,
 }  // namespace
 
 extern "C" int32_t celty_default_tile_rows(int32_t M, int32_t K) {
-  (void)K;
   if (M < 1) return 0;
+  // wide matrices (K >= 4M) take tiles twice as tall: their merge traffic,
+  // which grows with M times the slices per tile, stays small next to the
+  // data, and the longer segments stream better
+  const int64_t span = static_cast<int64_t>(K) >= 4 * static_cast<int64_t>(M) ? M / 4 : M / 8;
   int32_t r = 256;
-  while (r < 2048 && 2 * r <= M / 8) r *= 2;
+  while (r < 2048 && 2 * r <= span) r *= 2;
   return r;
 }
 

@@ -53,10 +53,14 @@ def test_status_strings():
 
 
 def test_default_tile_rows():
-    # largest power of two <= M / 8, clamped to [256, 2048]
+    # largest power of two <= M / 8, clamped to [256, 2048] (K < 4 M)
     for M, want in [(1, 256), (1024, 256), (4096, 512), (4095, 256), (5120, 512), (8192, 1024), (11008, 1024),
                     (13824, 1024), (16384, 2048), (28672, 2048), (1 << 20, 2048)]:
         assert celty.default_tile_rows(M, 4096) == want, M
+    # wide matrices (K >= 4 M): largest power of two <= M / 4
+    for M, K, want in [(7168, 28672, 1024), (4096, 28672, 1024), (2048, 8192, 512), (1024, 8192, 256),
+                       (8192, 28672, 1024), (5120, 13824, 512), (4096, 16383, 512), (4096, 16384, 1024)]:
+        assert celty.default_tile_rows(M, K) == want, (M, K)
     assert celty._default_tile_rows(0, 5) == 0
 
 
