@@ -170,7 +170,8 @@ size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R);
 /*
  * Zero-fill a workspace (device) on `stream`.  A workspace must be zero-filled
  * once before its first use; every completed celty_spmspv call leaves it
- * zero-filled again.  Errors: EINVAL (null), EHIP.
+ * zero-filled again.  Any alignment and size; one fill kernel, no memset, so
+ * the call may be recorded in a graph.  Errors: EINVAL (null or size 0), EHIP.
  */
 celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
 

@@ -661,6 +661,20 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs b
                                 p, static_cast<int>(blockIdx.x));
 }
 
+// Zero-fills n bytes at p: the bytes before the first 8-byte boundary, then
+// whole 64-bit words, then the rest.  A kernel rather than a memset, so that
+// a caller may record it in a graph.
+__global__ __launch_bounds__(256) void zero_fill_kernel(unsigned char* p, size_t n) {
+  const size_t head = std::min(n, static_cast<size_t>((8u - (reinterpret_cast<uintptr_t>(p) & 7u)) & 7u));
+  const size_t words = (n - head) / 8;
+  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+  const size_t i0 = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (size_t i = i0; i < head; i += stride) p[i] = 0u;
+  unsigned long long* w = reinterpret_cast<unsigned long long*>(p + head);
+  for (size_t i = i0; i < words; i += stride) w[i] = 0ull;
+  for (size_t i = head + 8 * words + i0; i < n; i += stride) p[i] = 0u;
+}
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
@@ -860,9 +874,11 @@ extern "C" size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R) 
 
 extern "C" celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
   if (!workspace || workspace_bytes == 0) return CELTY_EINVAL;
-  return hipMemsetAsync(workspace, 0, workspace_bytes, static_cast<hipStream_t>(stream)) == hipSuccess
-             ? CELTY_OK
-             : CELTY_EHIP;
+  const size_t words = workspace_bytes / 8 + 1;
+  const unsigned blocks = static_cast<unsigned>(std::min<size_t>((words + 255) / 256, 1024));
+  hipLaunchKernelGGL(zero_fill_kernel, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<unsigned char*>(workspace), workspace_bytes);
+  return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
 }
 
 extern "C" celty_status celty_spmspv_plan(const celty_rlc_csc* W, const celty_launch* launch_cfg,

@@ -491,6 +491,48 @@ def test_graph_replays_match_eager(celty, torch_dev):
     _check(e1.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
 
 
+@pytest.mark.parametrize("offset,size", [(0, 8), (1, 1), (3, 1001), (5, 7), (0, 2048 * 8 + 3),
+                                         (7, 300000 * 8 + 5), (0, 1100000 * 8)])
+def test_workspace_init_fills_exactly_its_bytes(celty, torch_dev, offset, size):
+    torch, dev = torch_dev
+    _note(f"workspace_init offset={offset} size={size}")
+    buf = torch.full((offset + size + 16,), 0xAB, dtype=torch.uint8, device=dev)
+    celty.celty_spmspv_workspace_init(buf[offset:offset + size])
+    torch.cuda.synchronize()
+    h = buf.cpu().numpy()
+    assert np.all(h[offset:offset + size] == 0)
+    assert np.all(h[:offset] == 0xAB) and np.all(h[offset + size:] == 0xAB)
+
+
+def test_workspace_init_recorded_in_a_graph(celty, torch_dev):
+    # the init and the product captured together; between replays the
+    # workspace is overwritten with garbage by eager work, so every replay
+    # depends on the captured fill
+    torch, dev = torch_dev
+    _note("workspace_init in a graph")
+    p = workloads.random_small(803, 3000, 2000, ws=60, as_=50)
+    Wp = celty.celty_encode(p.W, p.mask, 512).to_device(dev)
+    xp = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    ws = celty.new_workspace(Wp, dev)
+    want = torch.empty(3000, dtype=torch.int16, device=dev)
+    celty.celty_spmspv(Wp, xp, p.tau, want, ws)
+    torch.cuda.synchronize()
+    y = torch.empty_like(want)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        celty.celty_spmspv_workspace_init(ws)
+        celty.celty_spmspv(Wp, xp, p.tau, y, ws)
+    for rep in range(4):
+        ws.fill_(0x5A)
+        y.fill_(0x7C01)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, want), f"replay {rep} differs"
+        assert int(ws.count_nonzero()) == 0
+    _check(want.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
+
+
 def test_two_streams_with_own_workspaces(celty, torch_dev):
     torch, dev = torch_dev
     _note("two streams")
