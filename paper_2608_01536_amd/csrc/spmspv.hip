@@ -32,7 +32,6 @@
 
 #include <algorithm>
 #include <atomic>
-#include <climits>
 #include <type_traits>
 #include <cmath>
 #include <cstdint>
@@ -95,13 +94,6 @@ __device__ __forceinline__ uint32_t row_inclusive_max(uint32_t v) {
   v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false)));
   return v;
 }
-__device__ __forceinline__ int row_suffix_min(int v) {   // lanes past the row end count as INT_MAX
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x101, 0xF, 0xF, false));   // row_shl:1
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x102, 0xF, 0xF, false));   // row_shl:2
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x104, 0xF, 0xF, false));   // row_shl:4
-  v = min(v, __builtin_amdgcn_update_dpp(INT_MAX, v, 0x108, 0xF, 0xF, false));   // row_shl:8
-  return v;
-}
 
 // Block-wide: exclusive scans of a and b, their totals, and the maximum of m
 // (WAVES <= 16).  Each wavefront's totals go to part[] (3*WAVES words, used
@@ -148,11 +140,29 @@ __device__ __forceinline__ int fixed_point_scale(uint32_t n_seg, float max_abs, 
   return min(max(30 - e, -64), 64);
 }
 
-// Wavefront of a segment starting at flat group offset off: non-decreasing in
-// off (rounding included), in [0, WAVES).
-template <int WAVES>
-__device__ __forceinline__ int wave_of(uint32_t off, float wscale) {
-  return min(static_cast<int>(static_cast<float>(off) * wscale), WAVES - 1);
+// 4 * sum of (run + 1) over the 8 entries of a group (runs word rw).
+__device__ __forceinline__ int group_span4(uint32_t rw) {
+  return static_cast<int>(__builtin_amdgcn_sad_u8(((rw << 2) & 0x3C3C3C3Cu) + ((rw >> 2) & 0x3C3C3C3Cu), 0u, 32u));
+}
+
+// The segment that holds flat group `at` (at < the slice's group count), for
+// a whole wavefront: the n_seg <= 64 * 64 segments, sorted by offset, are
+// searched with two ballots, over every stride-th segment and then over the
+// one bucket of stride segments that holds `at`.  Returns the segment's index
+// and its gstart, off and cnt (wavefront-uniform; xs is left 0).
+__device__ __forceinline__ int holding_segment(const SegInfo* seg, int n_seg, uint32_t at, int lane, SegInfo& r) {
+  const int stride = (n_seg + kWave - 1) / kWave;   // <= 64
+  const int s1 = min(lane * stride, n_seg - 1);
+  const int c1 = __popcll(__ballot(seg[s1].off <= at));   // >= 1: segment 0 starts at 0
+  const int lo = min((c1 - 1) * stride, n_seg - 1);
+  const int hi = min(c1 * stride, n_seg);
+  const SegInfo sg = seg[min(lo + lane, n_seg - 1)];
+  const int c2 = __popcll(__ballot(lo + lane < hi && sg.off <= at));   // >= 1
+  r.gstart = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sg.gstart), c2 - 1));
+  r.off = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sg.off), c2 - 1));
+  r.cnt = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sg.cnt), c2 - 1));
+  r.xs = 0.f;
+  return lo + c2 - 1;
 }
 
 // fp16 (low or high half of a word) times an fp32 value, in one mixed-precision
@@ -428,7 +438,6 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   SegInfo* seg = reinterpret_cast<SegInfo*>(smem + e.seg_off);
   int* scr_all = reinterpret_cast<int*>(smem + e.scr_off);
   uint32_t* part = reinterpret_cast<uint32_t*>(smem + e.misc_off);   // 3*WAVES
-  int* wfirst = reinterpret_cast<int*>(part + 3 * WAVES);             // WAVES
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int t = blk / e.KC, c = blk - t * e.KC;
@@ -468,13 +477,11 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
 
   for (int i = tid; i < e.tile_slots; i += NT) tile[i] = 0;
   for (int i = tid; i < NT * G; i += NT) scr_all[i] = 0;
-  if (tid < WAVES) wfirst[tid] = INT_MAX;
   int scale = 0;   // the workgroup's fixed-point scale 2^scale
 
   // ---- selection of this slice's active, non-empty columns ----------------
-  // The flat group sequence is then cut into one range per wavefront:
-  // segment i goes to wavefront wave_of(off_i), and wfirst[w] collects the
-  // lowest segment index of wavefront w (INT_MAX when none starts there).
+  // The flat group sequence is then cut into equal ranges, one per
+  // wavefront (a segment may be shared by several).
   uint32_t n_seg, n_grp;
   if (one_per_lane) {
     // one column per lane
@@ -487,11 +494,7 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     block_scan_select<WAVES>(keep ? 1u : 0u, cnt, keep ? __float_as_uint(fabsf(xv)) : 0u, en, eg, n_seg, n_grp,
                              xmax_bits, part);
     const int s = fixed_point_scale(n_seg, e.max_abs, xmax_bits);
-    const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
-    if (keep) {
-      seg[en] = SegInfo{g0, eg, cnt, ldexpf(xv, s)};
-      atomicMin(wfirst + wave_of<WAVES>(eg, wscale), static_cast<int>(en));
-    }
+    if (keep) seg[en] = SegInfo{g0, eg, cnt, ldexpf(xv, s)};
     scale = s;
   } else {
     // m <= kMaxCols consecutive columns per lane (loaded above), so one block
@@ -509,14 +512,12 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     uint32_t en, eg, xmax_bits;
     block_scan_select<WAVES>(n_loc, g_loc, m_loc, en, eg, n_seg, n_grp, xmax_bits, part);
     const int s = fixed_point_scale(n_seg, e.max_abs, xmax_bits);
-    const float wscale = n_grp ? static_cast<float>(WAVES) / static_cast<float>(n_grp) : 0.f;
     uint32_t idx = en, off = eg;
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) {
       if ((keep_bits >> j) & 1u) {
         const uint32_t cnt = g[j + 1] - g[j];
         seg[idx] = SegInfo{g[j], off, cnt, ldexpf(half_bits_to_float(xr[j]), s)};
-        atomicMin(wfirst + wave_of<WAVES>(off, wscale), static_cast<int>(idx));
         ++idx;
         off += cnt;
       }
@@ -532,22 +533,34 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // register copies force an early wait.  Passes past the end are idle (every
   // lane inactive, loads of group 0) and accumulate nothing.
   constexpr uint32_t P = kWave * G;
-  // wavefront wv walks the segments [i_begin, i_end): the first segment of
-  // any wavefront at or after wv (n_seg if none), up to that of wv + 1
-  // (lane l < WAVES reads wfirst[l]; a suffix minimum over the row)
-  int i_begin, i_end;
-  {
-    const int f = row_suffix_min(lane < WAVES ? wfirst[lane] : INT_MAX);
-    const int wvu = __builtin_amdgcn_readfirstlane(wv);
-    i_begin = min(static_cast<int>(n_seg), __builtin_amdgcn_readlane(f, wvu));
-    i_end = min(static_cast<int>(n_seg), __builtin_amdgcn_readlane(f, wvu + 1));
-  }
-  if (i_begin < i_end) {
+  // Wavefront wv walks the flat groups [pb0, pe) (w * n_grp < 2^31: n_grp <
+  // 2^27), starting in segment i_begin.  Segments past the range are never
+  // assigned to a live lane, so the walk's segment bound is simply n_seg.
+  const int wvu = __builtin_amdgcn_readfirstlane(wv);
+  const uint32_t pb0 = static_cast<uint32_t>(wvu) * n_grp / WAVES;
+  const uint32_t pe = static_cast<uint32_t>(wvu + 1) * n_grp / WAVES;
+  if (pb0 < pe) {
+    SegInfo s0;
+    const int i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
+    const int i_end = static_cast<int>(n_seg);
     const Streams st = make_streams(p.values, p.runs, p.n_groups);
     int* scr = scr_all + wv * kWave * G;
-    const uint32_t pb0 = seg[i_begin].off;
-    const uint32_t pe = i_end < static_cast<int>(n_seg) ? seg[i_end].off : n_grp;
     const int n_pass = static_cast<int>((pe - pb0 + P - 1) / P);
+    // A range that starts inside a segment starts at the row reached by the
+    // segment's earlier groups: their runs (up to 4 * 64 groups here, the
+    // rest below) are loaded ahead of the ring, so that their round trip
+    // overlaps the ring's.
+    const uint32_t before = pb0 - s0.off;
+    uint32_t rb[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (before > static_cast<uint32_t>(q * kWave)) {   // wavefront-uniform
+        // lanes past the earlier groups reread the last of them (their own
+        // lines, not one line shared by every wavefront)
+        const uint32_t j = min(static_cast<uint32_t>(q * kWave + lane), before - 1u);
+        rb[q] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + j) << 2), 0, 0);
+      }
+    }
     Pass<G> ring[DEPTH];
     uint32_t pf = pb0;    // flat start of the next pass to fetch
     int icur = i_begin;   // segment holding group pf
@@ -559,6 +572,17 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     }
     uint32_t pb = pb0;    // flat start of the pass being accumulated
     int carry = 0;        // 4 * sum of (run + 1) over its first segment's earlier groups
+    if (before > 0u) {
+      int acc = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc += static_cast<uint32_t>(q * kWave + lane) < before ? group_span4(rb[q]) : 0;
+      for (uint32_t j = 4 * kWave + lane; j - lane < before; j += kWave) {   // segments longer than 256 groups
+        const uint32_t rw =
+            __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + min(j, before - 1u)) << 2), 0, 0);
+        acc += j < before ? group_span4(rw) : 0;
+      }
+      carry = __builtin_amdgcn_readlane(wave_inclusive_scan(acc), kWave - 1);
+    }
     for (int done = 0; done < n_pass; done += DEPTH) {
 #pragma unroll
       for (int d = 0; d < DEPTH; ++d) {
@@ -740,7 +764,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   pl.scr_off = static_cast<int>(off);
   off += static_cast<size_t>(pl.waves) * kWave * pl.groups * 4;
   pl.misc_off = static_cast<int>(off);
-  off += static_cast<size_t>(4 * pl.waves + 1) * 4;
+  off += static_cast<size_t>(3 * pl.waves) * 4;   // the block scan's per-wavefront totals
   pl.lds = align_up(off, 16);
   if (pl.lds > static_cast<size_t>(kMaxLds)) return CELTY_EINVAL;
   pl.blocks = static_cast<int64_t>(W->T) * pl.KC;

@@ -283,6 +283,25 @@ def test_paper_kernel_shapes(celty, torch_dev, M, K, pct):
     _full(celty, torch_dev, p, f"paper shape {M}x{K} dual{pct}")
 
 
+@pytest.mark.parametrize("M,K,R,ws,launch", [
+    (4096, 40, 4096, 5, (40, 16, 1)),     # segments of ~490 groups: cuts more than 256 groups in
+    (4096, 40, 4096, 5, (40, 16, 4)),
+    (4096, 40, 4096, 5, (40, 2, 2)),
+    (8192, 3, 8192, 2, (3, 16, 1)),       # three segments of ~1000 groups, 16 ranges
+    (3000, 1, 3000, 10, (1, 16, 1)),      # one segment shared by every wavefront
+    (64, 2, 64, 50, (2, 16, 1)),          # fewer groups than wavefronts: empty ranges
+    (2000, 700, 1024, 20, (700, 8, 1)),   # several columns per lane, long segments
+])
+def test_wavefront_ranges_cut_inside_segments(celty, torch_dev, M, K, R, ws, launch):
+    # a workgroup's groups are split into equal ranges, one per wavefront, so
+    # a range can begin deep inside a segment and must start at the row that
+    # the segment's earlier groups reach
+    _note(f"ranges inside segments M={M} K={K} R={R} ws={ws} launch={launch}")
+    p = workloads.random_small(871 + K, M, K, ws=ws, as_=0)
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, -1.0, R, launch=launch)
+    _check(y, p.W, p.mask, p.x, -1.0)
+
+
 @pytest.mark.parametrize("M,R,launch", [
     (22016, 2048, None),             # last tile 1536 rows: two rows per lane, the second past the tile for half
     (2 * 4096 + 3000, 4096, (256, 16, 1)),   # last tile 3000 rows: four rows per lane
