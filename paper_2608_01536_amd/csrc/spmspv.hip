@@ -140,6 +140,24 @@ __device__ __forceinline__ int fixed_point_scale(uint32_t n_seg, float max_abs, 
   return min(max(30 - e, -64), 64);
 }
 
+// Start of wavefront w's range of the slice's n_grp groups.  A SIMD holds
+// wavefronts w, w + 4, ... and over a long walk serves its later ones more
+// slowly (with equal ranges, ranks w / 4 = 0..3 of 16 took 0.89, 0.94, 1.03
+// and 1.14 times the mean walk at 28672 x 8192), so with 16 wavefronts the
+// ranks get shares in proportion 70 : 66 : 62 : 58, in units of n_grp / 1024
+// (32-bit arithmetic: n_grp = 1024 q + m, n_grp < 2^27); otherwise equal
+// shares (w * n_grp < 2^31).
+template <int WAVES>
+__device__ __forceinline__ uint32_t cut_of(int w, uint32_t n_grp) {
+  if constexpr (WAVES == 16) {
+    const uint32_t r = static_cast<uint32_t>(w) >> 2, m = static_cast<uint32_t>(w) & 3u;
+    const uint32_t cum = 4u * (70u * r - 2u * r * (r - 1u)) + m * (70u - 4u * r);   // r(r-1) is even
+    return (n_grp >> 10) * cum + (((n_grp & 1023u) * cum) >> 10);
+  } else {
+    return static_cast<uint32_t>(w) * n_grp / WAVES;
+  }
+}
+
 // 4 * sum of (run + 1) over the 8 entries of a group (runs word rw).
 __device__ __forceinline__ int group_span4(uint32_t rw) {
   return static_cast<int>(__builtin_amdgcn_sad_u8(((rw << 2) & 0x3C3C3C3Cu) + ((rw >> 2) & 0x3C3C3C3Cu), 0u, 32u));
@@ -533,12 +551,11 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // register copies force an early wait.  Passes past the end are idle (every
   // lane inactive, loads of group 0) and accumulate nothing.
   constexpr uint32_t P = kWave * G;
-  // Wavefront wv walks the flat groups [pb0, pe) (w * n_grp < 2^31: n_grp <
-  // 2^27), starting in segment i_begin.  Segments past the range are never
+  // Wavefront wv walks the flat groups [pb0, pe), starting in segment i_begin.  Segments past the range are never
   // assigned to a live lane, so the walk's segment bound is simply n_seg.
   const int wvu = __builtin_amdgcn_readfirstlane(wv);
-  const uint32_t pb0 = static_cast<uint32_t>(wvu) * n_grp / WAVES;
-  const uint32_t pe = static_cast<uint32_t>(wvu + 1) * n_grp / WAVES;
+  const uint32_t pb0 = cut_of<WAVES>(wvu, n_grp);
+  const uint32_t pe = cut_of<WAVES>(wvu + 1, n_grp);
   if (pb0 < pe) {
     SegInfo s0;
     const int i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
