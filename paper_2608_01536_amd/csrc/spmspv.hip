@@ -752,11 +752,22 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   if (pl.waves != 2 && pl.waves != 4 && pl.waves != 8 && pl.waves != 16) return CELTY_EINVAL;
   int Kc = cfg ? cfg->cols_per_block : 0;
   if (Kc == 0) {
-    // about 4096 / waves workgroups: T row tiles times KC slices (at most
-    // 63, the merge's count byte) of a multiple of 64 columns
-    const int64_t target = 4096 / pl.waves;
-    const int64_t kcs = std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, (target + W->T / 2) / W->T));
+    // about 4096 / waves workgroups (16 wavefronts on each of 256 compute
+    // units): T row tiles times KC slices (at most 63, the merge's count
+    // byte) of a multiple of 64 columns
+    const int64_t slots = 4096 / pl.waves;
+    const int64_t kcs = std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, (slots + W->T / 2) / W->T));
     int64_t kc = ((W->K + kcs - 1) / kcs + 63) / 64 * 64;
+    const int64_t n_wg = W->T * ((W->K + kc - 1) / kc);
+    // Counts between one and two workgroups per compute unit leave some units
+    // with two and the rest with one, and counts past the slots start a
+    // second round: then take the most slices that fit the slots exactly,
+    // with no rounding of the width (up to one workgroup per unit, a count
+    // is kept: fewer, wider slices cost fewer merge tickets)
+    if (n_wg > slots || (pl.waves == 8 && n_wg > 256 && n_wg < slots)) {
+      const int64_t ks = std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, slots / W->T));
+      kc = (W->K + ks - 1) / ks;
+    }
     kc = std::min<int64_t>(kc, std::min(4096, kMaxCols * kWave * pl.waves));
     Kc = static_cast<int>(kc);
   }
