@@ -155,19 +155,29 @@ def _desc(M=4096, K=4096, R=256, G=1000):
 @host_only
 def test_automatic_plan_fills_the_compute_units_in_one_even_round():
     # 256 compute units, 16 wavefront slots each: the automatic shape never
-    # starts a second round of workgroups, and with 8-wavefront workgroups it
-    # either stays at one per unit or fills at least 90 % of two per unit
+    # starts a second round of workgroups; an 8-wavefront count between one
+    # and 0.9 x two per unit is either widened to fill the slots or kept as
+    # the rounded shape (64-column multiples) when its slices would be light
+    def plan(M, K, G):
+        R = celty.default_tile_rows(M, K)
+        d = _desc(M, K, R, G)
+        out, nb = celty_launch(), ctypes.c_int64()
+        assert celty._plan(ctypes.byref(d), None, ctypes.byref(out), ctypes.byref(nb), None) == CELTY_OK
+        return d, out, nb.value
     for M in (512, 1024, 3000, 4096, 5120, 7168, 8192, 10240, 11008, 13824, 15360, 22016, 28672, 57344):
         for K in (1000, 2048, 4096, 5120, 7168, 8192, 11008, 13824, 28672):
-            R = celty.default_tile_rows(M, K)
-            d = _desc(M, K, R)
-            out, nb = celty_launch(), ctypes.c_int64()
-            assert celty._plan(ctypes.byref(d), None, ctypes.byref(out), ctypes.byref(nb), None) == CELTY_OK
-            slots = 4096 // out.waves_per_block
-            KC = -(-K // out.cols_per_block)
-            assert nb.value == d.T * KC <= slots, (M, K, nb.value)
-            if out.waves_per_block == 8 and nb.value > 256:
-                assert nb.value >= 0.9 * slots or KC == 63 or KC == K, (M, K, nb.value)
+            for G in (1000, M * K // 16):
+                d, out, n = plan(M, K, G)
+                slots = 4096 // out.waves_per_block
+                KC = -(-K // out.cols_per_block)
+                assert n == d.T * KC <= slots, (M, K, G, n)
+                if out.waves_per_block == 8 and 256 < n < 0.9 * slots:
+                    assert out.cols_per_block % 64 == 0 or out.cols_per_block == K or KC == 63, (M, K, G, n)
+    # 5120 x 13824 at half density: 10 tiles x 51 slices; 5120 x 5120 with
+    # little stored data keeps 10 x 40
+    assert plan(5120, 13824, 5120 * 13824 // 16)[2] == 510
+    assert plan(5120, 5120, 1000)[2] == 400
+    assert plan(5120, 5120, 5120 * 5120 // 16)[2] == 510
 
 
 @host_only
