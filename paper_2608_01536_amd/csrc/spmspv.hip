@@ -144,14 +144,18 @@ __device__ __forceinline__ int fixed_point_scale(uint32_t n_seg, float max_abs, 
 // wavefronts w, w + 4, ... and over a long walk serves its later ones more
 // slowly (with equal ranges, ranks w / 4 = 0..3 of 16 took 0.89, 0.94, 1.03
 // and 1.14 times the mean walk at 28672 x 8192), so with 16 wavefronts the
-// ranks get shares in proportion 70 : 66 : 62 : 58, in units of n_grp / 1024
-// (32-bit arithmetic: n_grp = 1024 q + m, n_grp < 2^27); otherwise equal
-// shares (w * n_grp < 2^31).
+// ranks get shares in proportion 80 : 72 : 56 : 48 (the best of a measured
+// series; the speeds shift as the shares do), in units of n_grp / 1024:
+// rank r's weight is byte r of 0x30384850 and the weight of the ranks
+// below it is 16-bit field r of 0x340026001400000.  32-bit arithmetic (n_grp =
+// 1024 q + m, n_grp < 2^27); otherwise equal shares (w * n_grp < 2^31).
 template <int WAVES>
 __device__ __forceinline__ uint32_t cut_of(int w, uint32_t n_grp) {
   if constexpr (WAVES == 16) {
     const uint32_t r = static_cast<uint32_t>(w) >> 2, m = static_cast<uint32_t>(w) & 3u;
-    const uint32_t cum = 4u * (70u * r - 2u * r * (r - 1u)) + m * (70u - 4u * r);   // r(r-1) is even
+    const uint32_t wt = (0x30384850u >> (8u * (r & 3u))) & 255u;
+    const uint32_t below = r >= 4u ? 1024u : static_cast<uint32_t>(0x340026001400000ull >> (16u * r)) & 65535u;
+    const uint32_t cum = below + m * wt;
     return (n_grp >> 10) * cum + (((n_grp & 1023u) * cum) >> 10);
   } else {
     return static_cast<uint32_t>(w) * n_grp / WAVES;
