@@ -6,8 +6,11 @@
 //     counts: Section 3.1's column skip turned into stream compaction) and
 //     drops columns whose segment in tile t is empty;
 //   * the workgroup's compressed groups (8 entries = 16 B of fp16 values +
-//     4 B of packed 4-bit runs) form one flat sequence; it is cut at segment
-//     boundaries into one contiguous range per wavefront;
+//     4 B of packed 4-bit runs) form one flat sequence, cut at group
+//     boundaries into one contiguous range per wavefront (a segment may be
+//     shared; a range that starts inside one first sums the runs of its
+//     earlier groups to find its starting row; 16 wavefronts get shares
+//     weighted by their rank on the SIMD);
 //   * a wavefront walks its range 64*G groups per pass, keeping a ring of
 //     passes in flight: each lane loads its groups with 128-bit and 32-bit
 //     buffer loads (Section 3.1), turns the 8 runs of a group into 8
