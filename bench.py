@@ -43,10 +43,37 @@ def traffic_file(workload_key: str) -> str:
     return os.path.join(PROFILES, f"spmspv_{workload_key}_traffic.json")
 
 
+def kernel_source_code(text: str) -> str:
+    """The kernel source with comments removed and whitespace collapsed
+    (string and character literals kept as they are)."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        ch = text[i]
+        if text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif ch in "\"'":
+            j = i + 1
+            while j < n and text[j] != ch:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        else:
+            out.append(ch)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_sha() -> str:
+    """sha256 of the kernel source's code: a comment edit does not void the
+    counter profiles, a code edit does."""
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    with open(KERNEL_SOURCE, encoding="utf-8") as f:
+        return hashlib.sha256(kernel_source_code(f.read()).encode()).hexdigest()
 
 
 def measured_traffic(workload_key: str):

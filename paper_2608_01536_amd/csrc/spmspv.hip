@@ -558,8 +558,9 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // register copies force an early wait.  Passes past the end are idle (every
   // lane inactive, loads of group 0) and accumulate nothing.
   constexpr uint32_t P = kWave * G;
-  // Wavefront wv walks the flat groups [pb0, pe), starting in segment i_begin.  Segments past the range are never
-  // assigned to a live lane, so the walk's segment bound is simply n_seg.
+  // Wavefront wv walks the flat groups [pb0, pe), starting in segment
+  // i_begin.  Segments past the range are never assigned to a live lane, so
+  // the walk's segment bound is simply n_seg.
   const int wvu = __builtin_amdgcn_readfirstlane(wv);
   const uint32_t pb0 = cut_of<WAVES>(wvu, n_grp);
   const uint32_t pe = cut_of<WAVES>(wvu + 1, n_grp);

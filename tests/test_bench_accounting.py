@@ -20,3 +20,14 @@ def test_bench_bytes_match_oracle(M, K, R, ws, as_):
     act = spmspv.select_active(p.x, p.tau)
     assert e_a == accounting.active_entries(o, act)
     assert g_a == accounting.active_groups(o, act)
+
+
+def test_kernel_code_hash_ignores_comments_only():
+    # the counter profiles are keyed by the kernel's code: comments and
+    # whitespace do not count, string literals (inline assembly) and code do
+    src = 'int a = 1; // note\n/* block\n comment */ asm("ds_add_u32 %0 // x"); char c = \'"\';\n'
+    code = bench.kernel_source_code(src)
+    assert code == 'int a = 1; asm("ds_add_u32 %0 // x"); char c = \'"\';'
+    assert bench.kernel_source_code(src.replace("// note", "// other note\n\n")) == code
+    assert bench.kernel_source_code(src.replace("a = 1", "a = 2")) != code
+    assert bench.kernel_source_code('s = "a\\"b // c";') == 's = "a\\"b // c";'
