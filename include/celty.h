@@ -146,7 +146,9 @@ celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int
 /* Launch shape of celty_spmspv_ex.  Zero fields mean "choose automatically":
  * 16 wavefronts per workgroup for R >= 1024, else 8; slices sized for about
  * 4096 / waves_per_block workgroups (16 wavefronts on each of 256 compute
- * units); one group per lane.  The K columns are cut into
+ * units), never more, and widened to fill two 8-wavefront workgroups per
+ * unit evenly when the rounded width would load the units unevenly and the
+ * slices stay heavy enough; one group per lane.  The K columns are cut into
  * ceil(K / cols_per_block) slices, at most 63 (the merge counts slices in one
  * byte of a 64-bit word).  A workgroup's lanes scan at most 8 columns each:
  * cols_per_block <= 512 * waves_per_block. */
