@@ -814,6 +814,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
 // The launch: products, the largest per-product grid and LDS footprint.
 struct Launch {
   int waves = 8, groups = 1, n = 0;
+  bool shallow = false;   // one group per lane with a ring of two passes instead of three
   int64_t max_blocks = 0;
   size_t lds = 0;
 };
@@ -856,7 +857,7 @@ celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stre
 template <int WAVES>
 celty_status launch_groups(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
   switch (ln.groups) {
-    case 1: return launch_shape<WAVES, 1, 3>(ln, a, stream);
+    case 1: return ln.shallow ? launch_shape<WAVES, 1, 2>(ln, a, stream) : launch_shape<WAVES, 1, 3>(ln, a, stream);
     case 2: return launch_shape<WAVES, 2, 2>(ln, a, stream);
     case 4: return launch_shape<WAVES, 4, 2>(ln, a, stream);
     default: return CELTY_EINVAL;
@@ -995,6 +996,8 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
 
   BatchArgs ba{};
   ln.n = n;
+  int64_t total_blocks = 0;
+  double stored_groups = 0.0;
   size_t ws_off = 0;
   for (int i = 0; i < n; ++i) {
     Plan pl;
@@ -1005,6 +1008,8 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
     ba.blocks[i] = static_cast<int>(pl.blocks);   // make_plan keeps it below 2^31
     ln.max_blocks = std::max(ln.max_blocks, pl.blocks);
     ln.lds = std::max(ln.lds, pl.lds);
+    total_blocks += pl.blocks;
+    stored_groups += static_cast<double>(W[i]->n_groups);
   }
   // every y is written while the other products read their x; none may
   // overlap another product's x or y, or the workspace
@@ -1018,6 +1023,14 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
       if (overlaps(y[i], yb, y[j], 2u * static_cast<size_t>(W[j]->M))) return CELTY_EINVAL;
     }
   }
+  // Ring depth: with two 8-wavefront workgroups on a compute unit, two passes
+  // in flight per wavefront suffice, and walks of a few to a dozen passes
+  // run faster with two than with three; one workgroup per unit, and
+  // 16-wavefront workgroups, keep three.  The pass count is estimated with
+  // half of the stored groups active (the activation is not known here).
+  const double passes =
+      total_blocks > 0 ? 0.5 * stored_groups / (static_cast<double>(total_blocks) * ln.waves * kWave) : 0.0;
+  ln.shallow = ln.groups == 1 && ln.waves == 8 && total_blocks > 256 && passes >= 4.0 && passes <= 16.0;
   return launch(ln, ba, static_cast<hipStream_t>(stream));
 }
 
