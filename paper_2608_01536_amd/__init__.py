@@ -192,9 +192,17 @@ def _stream_handle(stream) -> Optional[int]:
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _dev_ptr(t, nbytes_each: int, name: str) -> int:
+def _dev_ptr(t, nbytes_each: int, name: str, min_numel: int = 0, device=None) -> int:
+    """Device address of t after the checks the C ABI cannot make itself: the
+    library takes bare pointers and trusts the sizes (x holds K halves, y M,
+    idx K ints), so a short or misplaced tensor is rejected here, before any
+    launch, rather than read or written out of bounds on the GPU."""
     if not t.is_cuda or not t.is_contiguous() or t.element_size() != nbytes_each:
         raise ValueError(f"{name} must be a contiguous CUDA tensor of {nbytes_each}-byte elements")
+    if t.numel() < min_numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, fewer than the {min_numel} the call uses")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the encoded matrix on {device}")
     return int(t.data_ptr())
 
 
@@ -253,8 +261,8 @@ def new_workspace(W: DeviceRlcCsc, device=None):
 
 def celty_select(x, tau: float, idx, count, stream=None) -> None:
     K = x.numel()
-    _check(_select(_dev_ptr(x, 2, "x"), K, float(tau), _dev_ptr(idx, 4, "idx"), _dev_ptr(count, 4, "count"),
-                   _stream_handle(stream)), "celty_select")
+    _check(_select(_dev_ptr(x, 2, "x"), K, float(tau), _dev_ptr(idx, 4, "idx", K, x.device),
+                   _dev_ptr(count, 4, "count", 1, x.device), _stream_handle(stream)), "celty_select")
 
 
 def _launch_struct(launch) -> Optional[celty_launch]:
@@ -268,17 +276,17 @@ def _launch_struct(launch) -> Optional[celty_launch]:
 
 
 def celty_spmspv(W: DeviceRlcCsc, x, tau: float, y, workspace, stream=None) -> None:
-    d = W.desc()
-    _check(_spmspv(ctypes.byref(d), _dev_ptr(x, 2, "x"), float(tau), _dev_ptr(y, 2, "y"),
-                   _dev_ptr(workspace, 1, "workspace"), workspace.numel(), _stream_handle(stream)),
+    d, dev = W.desc(), W.gptr.device
+    _check(_spmspv(ctypes.byref(d), _dev_ptr(x, 2, "x", W.K, dev), float(tau), _dev_ptr(y, 2, "y", W.M, dev),
+                   _dev_ptr(workspace, 1, "workspace", 0, dev), workspace.numel(), _stream_handle(stream)),
            "celty_spmspv")
 
 
 def celty_spmspv_ex(W: DeviceRlcCsc, x, tau: float, y, workspace, launch=None, stream=None) -> None:
-    d = W.desc()
+    d, dev = W.desc(), W.gptr.device
     ls = _launch_struct(launch)
-    _check(_spmspv_ex(ctypes.byref(d), _dev_ptr(x, 2, "x"), float(tau), _dev_ptr(y, 2, "y"),
-                      _dev_ptr(workspace, 1, "workspace"), workspace.numel(),
+    _check(_spmspv_ex(ctypes.byref(d), _dev_ptr(x, 2, "x", W.K, dev), float(tau), _dev_ptr(y, 2, "y", W.M, dev),
+                      _dev_ptr(workspace, 1, "workspace", 0, dev), workspace.numel(),
                       None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_ex")
 
 
@@ -306,11 +314,12 @@ def celty_spmspv_batch(Ws, xs, taus, ys, workspace, launch=None, stream=None) ->
     if not (len(xs) == len(taus) == len(ys) == n):
         raise ValueError("Ws, xs, taus and ys must have the same length")
     descs, arr = _desc_array(Ws)
-    xp = (_p * n)(*[_dev_ptr(x, 2, "x") for x in xs])
-    yp = (_p * n)(*[_dev_ptr(y, 2, "y") for y in ys])
+    xp = (_p * n)(*[_dev_ptr(x, 2, f"xs[{i}]", W.K, W.gptr.device) for i, (W, x) in enumerate(zip(Ws, xs))])
+    yp = (_p * n)(*[_dev_ptr(y, 2, f"ys[{i}]", W.M, W.gptr.device) for i, (W, y) in enumerate(zip(Ws, ys))])
     tp = (_f32 * n)(*[float(t) for t in taus])
     ls = _launch_struct(launch)
-    _check(_batch(n, arr, xp, tp, yp, _dev_ptr(workspace, 1, "workspace"), workspace.numel(),
+    dev = Ws[0].gptr.device if n else None
+    _check(_batch(n, arr, xp, tp, yp, _dev_ptr(workspace, 1, "workspace", 0, dev), workspace.numel(),
                   None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_batch")
 
 

@@ -373,3 +373,66 @@ def test_product_path_does_not_use_the_oracle():
                 text = open(os.path.join(dirpath, name)).read()
                 assert not re.search(r"^\s*(import|from)\s+oracle\b", text, flags=re.M), name
                 assert "oracle/" not in text and "oracle." not in text, name
+
+
+class _FakeDeviceTensor:
+    """Stands in for a contiguous CUDA tensor in the binding's argument checks
+    (its address is never passed on: each case below fails a check first)."""
+
+    is_cuda = True
+
+    def __init__(self, numel, element_size, device="cuda:0"):
+        self._n, self._e, self.device = numel, element_size, device
+
+    def is_contiguous(self):
+        return True
+
+    def element_size(self):
+        return self._e
+
+    def numel(self):
+        return self._n
+
+    def data_ptr(self):
+        return FAKE
+
+
+class _FakeEncoded:
+    def __init__(self, M, K, device="cuda:0"):
+        self.M, self.K = M, K
+        self.gptr = _FakeDeviceTensor(1, 4, device)
+
+    def desc(self):
+        return celty_rlc_csc()
+
+
+@host_only
+@pytest.mark.parametrize("case", ["x_short", "y_short", "x_device", "y_device", "ws_device"])
+def test_binding_rejects_short_or_misplaced_tensors(case):
+    """The C ABI takes bare pointers and trusts x to hold K halves and y M, so
+    the binding checks the tensors' sizes and device before calling it."""
+    M, K = 300, 200
+    W = _FakeEncoded(M, K)
+    x = _FakeDeviceTensor(K - 1 if case == "x_short" else K, 2, "cuda:1" if case == "x_device" else "cuda:0")
+    y = _FakeDeviceTensor(M - 1 if case == "y_short" else M, 2, "cuda:1" if case == "y_device" else "cuda:0")
+    ws = _FakeDeviceTensor(1 << 20, 1, "cuda:1" if case == "ws_device" else "cuda:0")
+    with pytest.raises(ValueError):
+        celty.celty_spmspv(W, x, 0.5, y, ws, stream=0)
+    with pytest.raises(ValueError):
+        celty.celty_spmspv_ex(W, x, 0.5, y, ws, (64, 4, 1), stream=0)
+    W2 = _FakeEncoded(M // 2, K)
+    x2 = _FakeDeviceTensor(K, 2)
+    y2 = _FakeDeviceTensor(M // 2, 2)
+    with pytest.raises(ValueError):   # the faulty pair second, so that every element is checked
+        celty.celty_spmspv_batch([W2, W], [x2, x], [0.5, 0.5], [y2, y], ws, stream=0)
+
+
+@host_only
+@pytest.mark.parametrize("case", ["idx_short", "count_empty", "idx_device"])
+def test_select_binding_rejects_short_or_misplaced_outputs(case):
+    K = 1000
+    x = _FakeDeviceTensor(K, 2)
+    idx = _FakeDeviceTensor(K - 1 if case == "idx_short" else K, 4, "cuda:1" if case == "idx_device" else "cuda:0")
+    count = _FakeDeviceTensor(0 if case == "count_empty" else 1, 4)
+    with pytest.raises(ValueError):
+        celty.celty_select(x, 0.5, idx, count, stream=0)

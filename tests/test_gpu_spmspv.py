@@ -188,6 +188,33 @@ def test_empty_matrix(celty, torch_dev):
     assert np.all(y.view(np.uint16) == 0)
 
 
+def test_short_tensors_are_rejected_before_any_launch(celty, torch_dev):
+    """x shorter than K or y shorter than M raise in the binding; y keeps its
+    contents (nothing was launched) and a correct call afterwards still works."""
+    torch, dev = torch_dev
+    p = workloads.random_small(21, 300, 200, ws=50, as_=50)
+    Wd = celty.celty_encode(p.W, p.mask, 64).to_device(dev)
+    ws = celty.new_workspace(Wd, dev)
+    xt = torch.from_numpy(np.ascontiguousarray(p.x).view(np.int16)).to(dev)
+    y = torch.full((300,), 0x7C01, dtype=torch.int16, device=dev)
+    _note("short x / short y rejected")
+    with pytest.raises(ValueError):
+        celty.celty_spmspv(Wd, xt[:199], p.tau, y, ws)
+    with pytest.raises(ValueError):
+        celty.celty_spmspv(Wd, xt, p.tau, y[:299], ws)
+    with pytest.raises(ValueError):
+        celty.celty_spmspv_batch([Wd, Wd], [xt, xt[:150]], [p.tau, p.tau], [y, y], celty.new_batch_workspace([Wd, Wd]))
+    idx = torch.empty(199, dtype=torch.int32, device=dev)
+    with pytest.raises(ValueError):
+        celty.celty_select(xt, p.tau, idx, torch.empty(1, dtype=torch.int32, device=dev))
+    torch.cuda.synchronize()
+    assert bool((y == 0x7C01).all())
+    celty.celty_spmspv(Wd, xt, p.tau, y, ws)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().view(np.float16).astype(np.float64)
+    assert ref.rel_error(got, ref.spmspv_dense_fp64(p.W, p.mask, p.x, p.tau)) <= TOL
+
+
 def test_weight_only_full_mask_is_dense_gemv(celty, torch_dev):
     rng = np.random.default_rng(12)
     M, K = 1024, 768
