@@ -134,6 +134,34 @@ def test_spmspv_fuzz(celty, torch_dev, M, K, R, ws, as_, groups):
     _check(y, p.W, p.mask, p.x, p.tau)
 
 
+def _random_plan_cases(n=40, seed=2608):
+    """Seeded shapes between the fixed lists: log-uniform M and K (at most
+    3e7 entries, so that the oracle stays fast), the library's tile height or
+    a random power of two, and sparsities from 30 to 85 %."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        M = int(np.exp(rng.uniform(np.log(48), np.log(30000))))
+        K = int(np.exp(rng.uniform(np.log(48), np.log(30000))))
+        if M * K > 30_000_000:
+            continue
+        R = int(2 ** rng.integers(6, 13)) if rng.random() < 0.5 else 0
+        ws, as_ = (int(v) for v in rng.integers(30, 86, size=2))
+        cases.append((M, K, R, ws, as_))
+    return cases
+
+
+@pytest.mark.parametrize("M,K,R,ws,as_", _random_plan_cases())
+def test_automatic_plan_random_shapes(celty, torch_dev, M, K, R, ws, as_):
+    """The automatic launch (workgroup count, slice width, wavefronts, ring
+    depth) on seeded shapes that no other test names, against the oracle."""
+    R = R or celty.default_tile_rows(M, K)
+    _note(f"auto plan M={M} K={K} R={R} ws={ws} as={as_}")
+    p = workloads.random_small(M + 3 * K + R, M, K, ws=ws, as_=as_)
+    y = _run(celty, torch_dev, p.W, p.mask, p.x, p.tau, R)
+    _check(y, p.W, p.mask, p.x, p.tau)
+
+
 # cols / (64 * waves) covers 1 to 8 columns per lane in the selection
 @pytest.mark.parametrize("launch", [(40, 2, 1), (41, 4, 2), (64, 2, 4), (64, 4, 1), (128, 8, 2), (256, 16, 4),
                                     (1000, 4, 1), (1000, 4, 4), (2048, 4, 2), (4096, 16, 1), (700, 8, 4),
