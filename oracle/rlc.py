@@ -23,7 +23,11 @@ Readings where the paper is silent (the same list is kept with the design notes)
 * each segment is padded to a multiple of 8 entries with (value 0, run 0)
   "dead" entries so that every 8-entry group starts 16-byte aligned;
 * values and runs are separate arrays; the 8 runs of a group are packed in one
-  32-bit word, entry j of the group in bits [4j, 4j+4).
+  32-bit word, entry j of the group in bits [4j, 4j+4);
+* colmax[k] holds the fp16 bit pattern of the largest |stored value| of column
+  k (+0 when the column stores nothing).  It is not part of the paper's
+  format; the GPU product derives its fixed-point scales from it, so the
+  encoder must produce it bit for bit.
 """
 from __future__ import annotations
 
@@ -119,6 +123,7 @@ class RlcCsc:
     seg_n: np.ndarray     # int64 [T*K], entries per segment before alignment
     n_nnz: int
     n_pad: int
+    colmax: np.ndarray    # uint16 [K], fp16 bits of the largest |stored value| per column
 
     @property
     def n_groups(self) -> int:
@@ -143,7 +148,8 @@ def encode_matrix(W: np.ndarray, mask, R: int) -> RlcCsc:
     Steps, in order: (1) stored set per segment; (2) gap before each stored
     entry, counted from the tile start or the previous stored entry;
     (3) greedy padding: gap // 16 entries (0, 15) then the value with run
-    gap % 16; (4) alignment of each segment to 8 entries; (5) packing.
+    gap % 16; (4) alignment of each segment to 8 entries; (5) packing;
+    (6) the column maxima of the stored magnitudes.
     Vectorised over all stored entries; checked against a per-column call of
     rlc_encode_column in the tests.
     """
@@ -209,10 +215,21 @@ def encode_matrix(W: np.ndarray, mask, R: int) -> RlcCsc:
     for j in range(GROUP):
         packed |= re[:, j] << np.uint32(4 * j)
 
+    # (6) fp16 magnitudes order like their bit patterns with the sign cleared
+    colmax = column_max_bits(Wb, S)
+
     if G >= (1 << 32):
         raise OverflowError("group count does not fit in uint32")
     return RlcCsc(M=M, K=K, R=R, T=T, gptr=gptr.astype(np.uint32), values=values, runs=packed,
-                  seg_n=seg_n, n_nnz=int(S.sum()), n_pad=int(n_padding.sum()))
+                  seg_n=seg_n, n_nnz=int(S.sum()), n_pad=int(n_padding.sum()), colmax=colmax)
+
+
+def column_max_bits(W_bits: np.ndarray, stored: np.ndarray) -> np.ndarray:
+    """uint16 [K]: bits of max |W[r, k]| over the stored r of column k (0 if none)."""
+    mag = np.where(stored, np.asarray(W_bits, dtype=np.uint16) & np.uint16(0x7FFF), np.uint16(0))
+    if mag.shape[0] == 0:
+        return np.zeros(mag.shape[1], dtype=np.uint16)
+    return mag.max(axis=0).astype(np.uint16)
 
 
 def unpack_runs(runs: np.ndarray) -> np.ndarray:

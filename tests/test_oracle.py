@@ -331,3 +331,47 @@ def test_compression_ratio_4096_at_50pct():
     bm = accounting.bitmap_bytes(M, K, enc.n_nnz) / dense
     assert abs(bm - 0.5625) < 0.002
     assert round(bm * 100) == 56
+
+
+# --------------------------------------------------------------------------
+# Column maxima (the product's scale data) and the acceptance measure
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("M,K,R", [(1, 1, 1), (9, 5, 4), (70, 33, 16), (200, 57, 64)])
+def test_column_maxima_against_a_loop(M, K, R):
+    p = workloads.random_small(M * 31 + K, M, K, ws=60, as_=50, zero_weights=3)
+    Wb = p.W.view(np.uint16)
+    enc = rlc.encode_matrix(p.W, p.mask, R)
+    for k in range(K):
+        best = 0.0
+        for r in range(M):
+            if p.mask[r, k] and float(p.W[r, k]) != 0.0:
+                best = max(best, abs(float(p.W[r, k])))
+        assert float(enc.colmax[k:k + 1].view(np.float16)[0]) == best
+        assert (int(enc.colmax[k]) & 0x8000) == 0
+    assert int(enc.colmax.max()) == max([int(b) & 0x7FFF for b, m in zip(Wb.ravel(), p.mask.ravel()) if m], default=0)
+
+
+def test_column_maxima_hand_case():
+    W = np.array([[1, 0, -65504], [-3, 0.5, 2], [0, -0.0, 6.1e-5]], dtype=np.float16)
+    mask = np.array([[1, 1, 0], [1, 1, 1], [1, 1, 1]], dtype=np.uint8)
+    enc = rlc.encode_matrix(W, mask, 2)
+    # column 0: |-3|; column 1: 0.5 (the kept -0 is not stored); column 2: the
+    # masked -65504 does not count, 2 does
+    assert enc.colmax.view(np.float16).tolist() == [3.0, 0.5, 2.0]
+    assert rlc.encode_matrix(np.zeros((2, 2), np.float16), None, 1).colmax.tolist() == [0, 0]
+
+
+@pytest.mark.parametrize("y,ref,want", [
+    ([1, 2], [1, 2], 0.0),
+    ([1.5, 2], [1, 2], 0.2499998750000625),              # 0.5 / (2 + 1e-6)
+    ([-1, 0], [1, 0], 1.999998000002),                   # a sign slip counts twice the value
+    ([0, 3e-9], [0, 0], 0.003),                          # all-zero reference: the 1e-6 floor
+    ([0.1, 0, 0, 0], [0, 0, 0, 0.2], 0.9999950000249999),  # the largest deviation, not the mean
+    ([0, -3], [0, -4], 0.24999993750001562),             # magnitude of a negative reference
+    ([], [], 0.0),
+])
+def test_rel_error_hand_values(y, ref, want):
+    # expected values computed in exact rational arithmetic from the criterion
+    # max_r |y - y*| / (max_r |y*| + 1e-6)
+    got = spmspv.rel_error(np.array(y, dtype=np.float64), np.array(ref, dtype=np.float64))
+    assert got == pytest.approx(want, rel=1e-15, abs=0.0)
