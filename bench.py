@@ -9,7 +9,10 @@ single kernel launch).
 
 Cold cache: the encoded matrix is copied to enough distinct device buffers to
 exceed 1 GiB (beyond the 256 MiB Infinity Cache and the L2s) and the steps
-rotate over them, so every step streams its weights from HBM.
+rotate over them, so every step streams its weights from HBM; before every
+timed graph replay a 1 GiB buffer is overwritten (outside the timed events),
+so the first copies a replay reads are not left in a cache by the replay
+before it, whatever the step count.
 
 Printed (one JSON line): µs per SpMSpV (value, lower is better), effective
 GB/s on algorithmic bytes, the roofline of the kernel (HIP events around a
@@ -41,6 +44,10 @@ CALIBRATION_BYTES = 256 << 20
 
 def traffic_file(workload_key: str) -> str:
     return os.path.join(PROFILES, f"spmspv_{workload_key}_traffic.json")
+
+
+def kernel_trace_file(workload_key: str) -> str:
+    return os.path.join(PROFILES, f"spmspv_{workload_key}_kernel_trace.json")
 
 
 def kernel_source_code(text: str) -> str:
@@ -89,6 +96,49 @@ def measured_traffic(workload_key: str):
     return rec.get("traffic_bytes_per_launch")
 
 
+def recorded_kernel_trace(workload_key: str):
+    """Dispatch durations of the SpMSpV kernel from the committed kernel-trace
+    record, or None when it is missing, for another workload, or older than
+    the kernel."""
+    try:
+        with open(kernel_trace_file(workload_key)) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_sha() or rec.get("workload_key") != workload_key:
+        return None
+    return rec
+
+
+def record_kernel_trace(workload_key: str, trace_csv: str, command: str) -> int:
+    """Turns a rocprofv3 --kernel-trace CSV of this benchmark into the record
+    recorded_kernel_trace() reads: the mean and median duration of the
+    SpMSpV dispatches of the graph replays (the last 5 * steps dispatches:
+    the warm-up and eager calls come first)."""
+    import csv
+    import statistics
+    durs = []
+    with open(trace_csv) as f:
+        for row in csv.DictReader(f):
+            if "spmspv_kernel" in row["Kernel_Name"]:
+                durs.append((int(row["Start_Timestamp"]), int(row["End_Timestamp"]) - int(row["Start_Timestamp"])))
+    if not durs:
+        print("record-kernel-trace: no SpMSpV dispatches in the trace", file=sys.stderr)
+        return 1
+    durs.sort()
+    steps = int(command.split("--steps")[1].split()[0]) if "--steps" in command else 1000
+    tail = [d for _, d in durs[-5 * steps:]]
+    rec = {"workload_key": workload_key, "kernel_source_sha256": kernel_source_sha(),
+           "dispatches": len(tail), "mean_ns": round(statistics.fmean(tail), 1),
+           "median_ns": float(statistics.median(tail)), "min_ns": min(tail), "max_ns": max(tail),
+           "command": command}
+    with open(kernel_trace_file(workload_key), "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec))
+    return 0
+
+
 def _counter_per_dispatch(csv_path: str, name_parts) -> list:
     """Per-dispatch sums of a rocprofv3 counter CSV for kernels whose name
     contains any of name_parts."""
@@ -132,131 +182,169 @@ def record_traffic(workload_key: str, paths, commands) -> int:
     return 0
 
 
+def _encode_layer(job):
+    """Host worker: draw the 7 projections of one layer (its own seeds, x and
+    tau) and encode them; also the stacked encodings of the projections that
+    share an x (q/k/v, gate/up), which the fused schedule launches as one
+    taller matrix.  Returns plain host data for the parent to upload."""
+    cfg, layer, as_, fused = job
+    import paper_2608_01536_amd as celty
+    import workloads
+
+    probs = workloads.layer_problems(cfg, 0, layer, as_)
+    encs = [celty.celty_encode(p.W, p.mask, celty.default_tile_rows(*p.W.shape)) for p in probs]
+    alg = [algorithmic_bytes_from_encoding(e, p.x, p.tau)[0] for e, p in zip(encs, probs)]
+    groups = _x_groups(cfg)
+    xs = {workloads.CONFIGS[cfg]["layers"][g[0]].x_group: probs[g[0]].x for g in groups}
+    taus = [p.tau for p in probs]
+    stacked = []
+    if fused:
+        for g in groups:
+            if len(g) == 1:
+                stacked.append(None)
+                continue
+            Wst = np.concatenate([probs[i].W for i in g], axis=0)
+            Mst = np.concatenate([probs[i].mask for i in g], axis=0)
+            stacked.append(celty.celty_encode(Wst, Mst, celty.default_tile_rows(*Wst.shape)))
+            del Wst, Mst
+    dense_shapes = [p.W.shape for p in probs]
+    del probs
+    return layer, encs, stacked, xs, taus, alg, dense_shapes
+
+
+def _x_groups(cfg):
+    """Runs of consecutive projections that read the same x."""
+    import workloads
+    groups, prev = [], None
+    for i, pr in enumerate(workloads.CONFIGS[cfg]["layers"]):
+        if pr.x_group == prev:
+            groups[-1].append(i)
+        else:
+            groups.append([i])
+        prev = pr.x_group
+    return groups
+
+
 def sequence_bench(args) -> int:
     """One decode step of config 3, 4 or 5: the 7 projections of every layer,
-    timed as one HIP graph per schedule.  Layers are distinct device copies of
-    layer 0's encodings (same values, separate memory), so every step streams
-    all of its weights from HBM; at least 1 GiB of copies is rotated when the
-    step itself is smaller."""
-    import torch
-    import torch.nn.functional as F
+    timed as one HIP graph per schedule.  Every layer is its own draw (seeds
+    per layer and projection, its own activations and thresholds), encoded on
+    the host by a pool of worker processes and uploaded to HBM, so a step
+    streams all of its distinct weights from HBM.  When the step moves less
+    than 1 GiB the graph runs it several times over (each time the caches are
+    overwritten before the timed replay)."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
 
-    import paper_2608_01536_amd as celty
     import workloads
 
     cfg = args.sequence
     c = workloads.CONFIGS[cfg]
     as_ = args.seq_as if args.seq_as is not None else (c["as_"] if not isinstance(c["as_"], tuple) else 60)
     n_layers = args.layers or c["n_layers"]
+    fused_on = not args.no_fused
+    groups = _x_groups(cfg)
+    names = [pr.name for pr in c["layers"]]
+    workers = max(1, min(args.workers or 16, len(os.sched_getaffinity(0)), n_layers))
+    print(f"[sequence] config {cfg}: {n_layers} distinct layers at as{as_:g}, {workers} host workers",
+          file=sys.stderr, flush=True)
+    # the pool starts before this process touches the GPU
+    pool = cf.ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("fork"))
+    futs = [pool.submit(_encode_layer, (cfg, l, as_, fused_on)) for l in range(n_layers)]
+
+    import torch
+    import torch.nn.functional as F
+
+    import paper_2608_01536_amd as celty
+
     dev = torch.device("cuda:0")
-    probs = workloads.layer_problems(cfg, 0, 0, as_)
-    names = [p.meta["proj_name"] for p in probs]
-    Rs = [celty.default_tile_rows(*p.W.shape) for p in probs]
-    encs = [celty.celty_encode(p.W, p.mask, R) for p, R in zip(probs, Rs)]
-    alg = [algorithmic_bytes_from_encoding(e, p.x, p.tau)[0] for e, p in zip(encs, probs)]
-    layer_bytes = sum(stored_bytes(e) for e in encs)
-    n_copies = max(n_layers, -(-COLD_BYTES // layer_bytes))
-    print(f"[sequence] config {cfg}: {n_layers} layers, as{as_:g}, {n_copies} device copies of "
-          f"{layer_bytes / 1e6:.1f} MB", file=sys.stderr, flush=True)
-    base = [e.to_device(dev) for e in encs]
-    del encs
-    layers = [base] + [[W.clone_to() for W in base] for _ in range(n_copies - 1)]
-    xg = {}
-    for p, pr in zip(probs, c["layers"]):
-        if pr.x_group not in xg:
-            xg[pr.x_group] = torch.from_numpy(p.x.view(np.int16)).to(dev)
-    xs = [xg[pr.x_group] for pr in c["layers"]]
-    taus = [p.tau for p in probs]
-    ys = [torch.empty(p.W.shape[0], dtype=torch.int16, device=dev) for p in probs]
-    wss = [celty.new_workspace(W, dev) for W in base]
-    # batched schedule: consecutive projections reading the same x share a launch
-    groups, prev = [], None
-    for i, pr in enumerate(c["layers"]):
-        if pr.x_group == prev:
-            groups[-1].append(i)
-        else:
-            groups.append([i])
-        prev = pr.x_group
-    bws = [celty.new_batch_workspace([base[i] for i in g], dev) for g in groups]
-    # fused schedule: the projections of a group (same x) stacked into one
-    # taller matrix at encode time (a fused q/k/v or gate/up weight), so one
-    # single-product launch computes all of them
-    fused_base = []
-    for g in groups:
-        if len(g) == 1:
-            fused_base.append(base[g[0]])
-            continue
-        Wst = np.concatenate([probs[i].W for i in g], axis=0)
-        Mst = np.concatenate([probs[i].mask for i in g], axis=0)
-        Rf = celty.default_tile_rows(*Wst.shape)
-        fused_base.append(celty.celty_encode(Wst, Mst, Rf).to_device(dev))
-        del Wst, Mst
-    fused_bytes = sum(stored_bytes(f.host_header) if hasattr(f, "host_header") else 0 for f in fused_base)
-    n_fcopies = max(n_layers, -(-COLD_BYTES // max(1, fused_bytes)))
-    fused_layers = [fused_base] + [[f.clone_to() for f in fused_base] for _ in range(n_fcopies - 1)]
-    fys = [torch.empty(f.M, dtype=torch.int16, device=dev) for f in fused_base]
-    fws = [celty.new_workspace(f, dev) for f in fused_base]
-    gx = [xs[g[0]] for g in groups]
-    gtau = [taus[g[0]] for g in groups]
-    steps = max(2, -(-n_copies // n_layers)) * 2
+    layers = [None] * n_layers          # per layer: device encodings of the 7 projections
+    fused = [None] * n_layers           # per layer: one device encoding per x-group
+    xs = [None] * n_layers              # per layer: device x of each projection
+    taus = [None] * n_layers
+    alg_step = 0.0
+    stored_step = 0
+    dense_shapes = None
+    done = 0
+    for fut in cf.as_completed(futs):
+        layer, encs, stacked, xh, tl, alg, dense_shapes = fut.result()
+        layers[layer] = [e.to_device(dev) for e in encs]
+        if fused_on:
+            fused[layer] = [layers[layer][g[0]] if st is None else st.to_device(dev)
+                            for g, st in zip(groups, stacked)]
+        xd = {k: torch.from_numpy(v.view(np.int16)).to(dev) for k, v in xh.items()}
+        xs[layer] = [xd[pr.x_group] for pr in c["layers"]]
+        taus[layer] = tl
+        alg_step += sum(alg)
+        stored_step += sum(stored_bytes(e) for e in encs)
+        del encs, stacked
+        done += 1
+        if done % 8 == 0 or done == n_layers:
+            print(f"[sequence] {done}/{n_layers} layers encoded and uploaded", file=sys.stderr, flush=True)
+    pool.shutdown()
+    flush = CacheFlush(torch)
+    ys = [torch.empty(pr.M, dtype=torch.int16, device=dev) for pr in c["layers"]]
+    wss = [celty.new_workspace(W, dev) for W in layers[0]]
+    bws = [celty.new_batch_workspace([layers[0][i] for i in g], dev) for g in groups]
+    if fused_on:
+        fys = [torch.empty(f.M, dtype=torch.int16, device=dev) for f in fused[0]]
+        fws = [celty.new_workspace(f, dev) for f in fused[0]]
+    # a step smaller than the cold threshold is repeated within one graph
+    reps = max(1, -(-COLD_BYTES // max(1, stored_step)))
 
     def step_sequential(s):
         for l in range(n_layers):
-            L = layers[(s * n_layers + l) % n_copies]
+            L = layers[l]
             for i in range(len(L)):
-                celty.celty_spmspv(L[i], xs[i], taus[i], ys[i], wss[i])
+                celty.celty_spmspv(L[i], xs[l][i], taus[l][i], ys[i], wss[i])
 
     def step_batched(s):
         for l in range(n_layers):
-            L = layers[(s * n_layers + l) % n_copies]
+            L = layers[l]
             for g, w in zip(groups, bws):
-                celty.celty_spmspv_batch([L[i] for i in g], [xs[i] for i in g], [taus[i] for i in g],
+                celty.celty_spmspv_batch([L[i] for i in g], [xs[l][i] for i in g], [taus[l][i] for i in g],
                                          [ys[i] for i in g], w)
 
     def step_fused(s):
         for l in range(n_layers):
-            L = fused_layers[(s * n_layers + l) % n_fcopies]
-            for j in range(len(L)):
-                celty.celty_spmspv(L[j], gx[j], gtau[j], fys[j], fws[j])
+            for j, g in enumerate(groups):
+                celty.celty_spmspv(fused[l][j], xs[l][g[0]], taus[l][g[0]], fys[j], fws[j])
 
     out = {"sequence": cfg, "name": c["name"], "activation_sparsity_pct": as_, "layers": n_layers,
-           "device_copies": n_copies, "data": "synthetic",
-           "alg_bytes_per_step": int(n_layers * sum(alg)), "stored_bytes_per_layer": int(layer_bytes)}
-    for label, fn, launches in (("sequential", step_sequential, len(names)), ("batched", step_batched, len(groups)),
-                                ("fused", step_fused, len(groups))):
+           "distinct_layers": True, "data": "synthetic",
+           "alg_bytes_per_step": int(alg_step), "stored_bytes_per_step": int(stored_step),
+           "graph_repeats_of_the_step": reps}
+    schedules = [("sequential", step_sequential, len(names)), ("batched", step_batched, len(groups))]
+    if fused_on:
+        schedules.append(("fused", step_fused, len(groups)))
+    for label, fn, launches in schedules:
         for i in range(2):
             fn(i)
         torch.cuda.synchronize()
-        us, samples = time_graph(torch, fn, steps, replays=3)
+        us, samples = time_graph(torch, fn, reps, replays=3, flush=flush)
         out[label] = {"us_per_step": round(us, 2), "launches_per_step": n_layers * launches,
-                      "GBps": round(out["alg_bytes_per_step"] / us / 1e3, 1),
-                      "pct_peak_hbm": round(100 * out["alg_bytes_per_step"] / us / 1e3 / PEAK_HBM_GBPS, 2)}
+                      "GBps": round(alg_step / us / 1e3, 1),
+                      "pct_peak_hbm": round(100 * alg_step / us / 1e3 / PEAK_HBM_GBPS, 2)}
         print(f"[sequence] {label}: {us:.1f} us/step", file=sys.stderr, flush=True)
-    per = {}
-    for i, nm in enumerate(names):
-        fn = lambda j, i=i: celty.celty_spmspv(layers[j % n_copies][i], xs[i], taus[i], ys[i], wss[i])
-        us, _ = time_graph(torch, fn, max(n_copies, 100), replays=3)
-        per[nm] = {"us": round(us, 3), "M": probs[i].W.shape[0], "K": probs[i].W.shape[1], "R": Rs[i],
-                   "GBps": round(alg[i] / us / 1e3, 1)}
-    out["per_projection"] = per
     if not args.no_dense:
         dense = {}
-        for i, nm in enumerate(names):
-            M, K = probs[i].W.shape
-            if (M, K) not in dense:
-                Wf = torch.from_numpy(np.where(probs[i].mask != 0, probs[i].W, np.float16(0))).to(dev)
-                nd = max(2, -(-COLD_BYTES // (2 * M * K)))
-                dc = [Wf] + [Wf.clone() for _ in range(nd - 1)]
-                xd = torch.zeros(1, K, dtype=torch.float16, device=dev)
-                for j in range(5):
-                    F.linear(xd, dc[j % nd])
-                dense[(M, K)], _ = time_graph(torch, lambda j: F.linear(xd, dc[j % nd]), max(nd, 100), replays=3)
-                del dc, Wf
-                torch.cuda.empty_cache()
-        d_step = n_layers * sum(dense[p.W.shape] for p in probs)
+        for (M, K) in sorted(set(dense_shapes)):
+            Wf = torch.zeros(M, K, dtype=torch.float16, device=dev)
+            Wf.normal_(0.0, 0.02)
+            nd = max(2, -(-COLD_BYTES // (2 * M * K)))
+            dc = [Wf] + [Wf.clone() for _ in range(nd - 1)]
+            xd = torch.zeros(1, K, dtype=torch.float16, device=dev)
+            for j in range(5):
+                F.linear(xd, dc[j % nd])
+            dense[(M, K)], _ = time_graph(torch, lambda j: F.linear(xd, dc[j % nd]), max(nd, 100), replays=3,
+                                          flush=flush)
+            del dc, Wf
+            torch.cuda.empty_cache()
+        d_step = n_layers * sum(dense[sh] for sh in dense_shapes)
         out["dense_gemv_us_per_step"] = round(d_step, 2)
-        out["dense_note"] = "sum over the layer's shapes of F.linear fp16 batch-1 times (cold copies) x layers"
-        out["speedup_vs_dense"] = {k: round(d_step / out[k]["us_per_step"], 3) for k in ("sequential", "batched", "fused")}
+        out["dense_note"] = ("sum over the layer's shapes of F.linear fp16 batch-1 times (cold copies, caches "
+                             "overwritten before each timed replay) x layers")
+        out["speedup_vs_dense"] = {k: round(d_step / out[k]["us_per_step"], 3) for k, _, _ in schedules}
     print(json.dumps(out))
     return 0
 
@@ -358,15 +446,20 @@ def fetched_bytes_from_encoding(enc, g_a: int, plan: dict) -> tuple:
     compressed: every 8-entry group of an active column's segments (16 B of
     values + 4 B of runs, the trailing alignment entries included) plus the
     group pointers (each workgroup reads the Kc + 1 pointers of its slice in
-    its row tile, so T * (K + KC) words).  total adds x, read once per row tile
-    (2 B * T * K), and y (2 B * M).  Returns (compressed, total)."""
+    its row tile, so T * (K + KC) words).  total adds x and the column maxima
+    of each workgroup's slice (2 + 2 B per column, once per row tile) and y
+    (2 B * M).  Returns (compressed, total, bound_pass): bound_pass is what
+    the workgroups read to sum the merge bound when there are several slices
+    (all of x and of the column maxima, 4 B * K each; L2 hits after the first
+    workgroup of an XCD)."""
     KC = -(-enc.K // plan["cols_per_block"])
     compressed = 20 * g_a + 4 * enc.T * (enc.K + KC)
-    return compressed, compressed + 2 * enc.T * enc.K + 2 * enc.M
+    bound_pass = 4 * enc.K * enc.T * KC if KC > 1 else 0
+    return compressed, compressed + 4 * enc.T * enc.K + 2 * enc.M, bound_pass
 
 
 def stored_bytes(enc) -> int:
-    return 2 * enc.values.size + 4 * enc.runs.size + 4 * enc.gptr.size
+    return 2 * enc.values.size + 4 * enc.runs.size + 4 * enc.gptr.size + 2 * enc.colmax.size
 
 
 def time_loop(torch, fn, steps: int) -> float:
@@ -381,20 +474,38 @@ def time_loop(torch, fn, steps: int) -> float:
     return s.elapsed_time(e) * 1e3 / steps
 
 
-def time_graph(torch, fn, steps: int, replays: int = 5) -> tuple:
+class CacheFlush:
+    """Overwrites COLD_BYTES of device memory: run before a timed replay
+    (outside its events), it evicts whatever the previous replay left in the
+    L2s and the Infinity Cache."""
+
+    def __init__(self, torch):
+        self.buf = torch.empty(COLD_BYTES, dtype=torch.uint8, device="cuda")
+        self.n = 0
+
+    def __call__(self):
+        self.n = (self.n + 1) & 0x7F
+        self.buf.fill_(self.n)
+
+
+def time_graph(torch, fn, steps: int, replays: int = 5, flush=None) -> tuple:
     """Capture `steps` calls in one HIP graph; return (µs per call of the timed
     replay, per-replay µs-per-call samples).  Replaying removes host launch
     overhead, so each call's time is its kernel plus the graph's inter-kernel
-    gap."""
+    gap.  flush, if given, runs before every replay, outside the timed events."""
     g = torch.cuda.CUDAGraph()
     torch.cuda.synchronize()
     with torch.cuda.graph(g):
         for i in range(steps):
             fn(i)
+    if flush is not None:
+        flush()
     g.replay()
     torch.cuda.synchronize()
     samples = []
     for _ in range(replays):
+        if flush is not None:
+            flush()
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.record()
         g.replay()
@@ -405,9 +516,10 @@ def time_graph(torch, fn, steps: int, replays: int = 5) -> tuple:
     return float(np.median(samples)), samples
 
 
-def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool = False) -> dict:
+def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool = False, flush=None) -> dict:
     """Graph-timed µs per celty_spmspv_ex call on rotated device copies of enc
-    (at least COLD_BYTES in all, so every call streams W from HBM)."""
+    (at least COLD_BYTES in all, so every call streams W from HBM; with
+    flush, the caches are also overwritten before every timed replay)."""
     dev = torch.device("cuda:0")
     ncopies = 1 if hot else max(2, -(-COLD_BYTES // stored_bytes(enc)))
     base = enc.to_device(dev)
@@ -427,16 +539,16 @@ def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool
     eager_us = time_loop(torch, step, steps)
     # the timed region: the steps captured in one HIP graph and replayed on
     # the launch stream; one step is exactly one kernel launch
-    us, samples = time_graph(torch, step, steps)
+    us, samples = time_graph(torch, step, steps, flush=None if hot else flush)
     out = {"us": us, "samples": samples, "eager_us": eager_us, "copies": ncopies}
     del copies, base
     torch.cuda.empty_cache()
     return out
 
 
-def cold_dense(torch, F, p, steps: int, hot: bool = False) -> dict:
+def cold_dense(torch, F, p, steps: int, hot: bool = False, flush=None) -> dict:
     """The dense reference: F.linear fp16 at batch 1 on the masked W and the
-    thresholded x, same cold rotation and graph timing."""
+    thresholded x, same cold rotation, cache overwrite and graph timing."""
     dev = torch.device("cuda:0")
     M, K = p.W.shape
     Wf = torch.from_numpy(np.where(p.mask != 0, p.W, np.float16(0))).to(dev)
@@ -446,7 +558,8 @@ def cold_dense(torch, F, p, steps: int, hot: bool = False) -> dict:
     for i in range(20):
         F.linear(xd, dcopies[i % nd])
     try:
-        dense_us, _ = time_graph(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps)
+        dense_us, _ = time_graph(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps,
+                                 flush=None if hot else flush)
         dense_mode = "graph"
     except Exception:
         dense_us, dense_mode = time_loop(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps), "eager"
@@ -481,9 +594,9 @@ def paper_shapes(args) -> int:
             enc = celty.celty_encode(p.W, p.mask, R)
             plan = celty.celty_spmspv_plan(enc, None)
             b_alg, _, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
-            comp, _ = fetched_bytes_from_encoding(enc, g_a, plan)
-            sp_ = cold_spmspv(torch, celty, enc, p, None, args.steps, args.warmup)
-            d = cold_dense(torch, F, p, args.steps)
+            comp, _, _ = fetched_bytes_from_encoding(enc, g_a, plan)
+            sp_ = cold_spmspv(torch, celty, enc, p, None, args.steps, args.warmup, flush=flush)
+            d = cold_dense(torch, F, p, args.steps, flush=flush)
             speed.setdefault(pct, []).append(d["us"] / sp_["us"])
             print(json.dumps({"M": M, "K": K, "dual_sparsity_pct": pct, "R": R, "launch": plan,
                               "us": round(sp_["us"], 3), "alg_GBps": round(b_alg / sp_["us"] / 1e3, 1),
@@ -558,10 +671,15 @@ def main() -> int:
                     help="only run a plain copy of a known size (counter calibration)")
     ap.add_argument("--record-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="host only: write this workload's HBM traffic record from rocprofv3 counter CSVs")
+    ap.add_argument("--record-kernel-trace", metavar="TRACE_CSV",
+                    help="host only: write this workload's kernel-duration record from a rocprofv3 "
+                         "--kernel-trace CSV of this benchmark run with the same flags")
     ap.add_argument("--sequence", type=int, choices=(3, 4, 5),
                     help="time one decode step of config 3, 4 or 5 (its own JSON line)")
     ap.add_argument("--layers", type=int, default=0, help="layers of --sequence (0 = the config's)")
     ap.add_argument("--seq-as", type=float, default=None, help="activation sparsity of --sequence")
+    ap.add_argument("--workers", type=int, default=0, help="host processes that encode --sequence layers (0 = 16)")
+    ap.add_argument("--no-fused", action="store_true", help="--sequence without the stacked-encoding schedule")
     ap.add_argument("--format-study", action="store_true",
                     help="host only: RLC-CSC vs bitmap vs dense sizes across weight sparsity")
     ap.add_argument("--paper-shapes", action="store_true",
@@ -613,11 +731,19 @@ def main() -> int:
         cmds += [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py --copy-calibration"
                  for c in ("FETCH_SIZE", "WRITE_SIZE")]
         return record_traffic(workload_key, args.record_traffic, cmds)
+    if args.record_kernel_trace:
+        flags = f" --M {M} --K {K} --ws {args.ws:g} --as {args.as_:g}" + (f" --R {args.R}" if args.R else "") + \
+                (f" --sigma {args.sigma:g}" if args.sigma else "") + \
+                (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "")
+        cmd = (f"rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o run -- python3 bench.py "
+               f"--no-cpu --no-dense --steps {args.steps} --warmup {args.warmup}{flags}")
+        return record_kernel_trace(workload_key, args.record_kernel_trace, cmd)
     dev = torch.device("cuda:0")
     b_alg, e_a, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
-    comp_fetched, total_fetched = fetched_bytes_from_encoding(enc, g_a, plan)
+    comp_fetched, total_fetched, bound_pass = fetched_bytes_from_encoding(enc, g_a, plan)
     print(f"[bench] {M}x{K} ws{args.ws:g} as{args.as_:g} R={R} plan={plan}", file=sys.stderr, flush=True)
-    run = cold_spmspv(torch, celty, enc, p, launch, args.steps, args.warmup, args.hot)
+    flush = None if args.hot else CacheFlush(torch)
+    run = cold_spmspv(torch, celty, enc, p, launch, args.steps, args.warmup, args.hot, flush=flush)
     us_step, samples, eager_us, ncopies = run["us"], run["samples"], run["eager_us"], run["copies"]
     us_kernel = us_step
     print(f"[bench] timed: {us_step:.3f} us/step (graph), eager {eager_us:.2f} us/call", file=sys.stderr, flush=True)
@@ -627,7 +753,7 @@ def main() -> int:
     floor_wall = time_loop(torch, lambda i: tiny.fill_(1.0), args.steps)
     floor_kernel, _ = time_graph(torch, lambda i: tiny.fill_(1.0), args.steps)
 
-    dense = None if args.no_dense else cold_dense(torch, F, p, args.steps, args.hot)
+    dense = None if args.no_dense else cold_dense(torch, F, p, args.steps, args.hot, flush=flush)
 
     cpu = None
     if not args.no_cpu:
@@ -637,6 +763,7 @@ def main() -> int:
     gbps_step = b_alg / us_step / 1e3
     achieved = b_alg / us_kernel / 1e3
     traffic = None if args.hot else measured_traffic(workload_key)
+    ktrace = None if args.hot else recorded_kernel_trace(workload_key)
     workload = (f"{M}x{K} fp16 W (out x in), {args.ws:g}% unstructured weight sparsity + "
                 f"{args.as_:g}% activation sparsity (Laplace x, magnitude threshold), batch 1")
     if args.sigma:
@@ -653,9 +780,10 @@ def main() -> int:
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
-        "arithmetic": "fp16 W and x; every product exact in fp32; sums in int32 fixed point per workgroup "
-                      "and int64 across column slices (at least as accurate as fp32 accumulation); y fp16 (RNE)",
+        "dtype": "f16 inputs, f32 products, i32/i64 fixed-point sums",
+        "arithmetic": "fp16 W and x; every product exact in fp32; sums in int32 fixed point per workgroup on a "
+                      "grid from the sum of colmax*|x| over its active columns, merged across column slices "
+                      "in int64 on a grid from the same sum over every active column; y fp16 (RNE)",
         "data": "synthetic",
         "config": {"workload": workload, "workload_key": workload_key, "M": M, "K": K, "weight_sparsity_pct": args.ws,
                    "activation_sparsity_pct": args.as_, "tile_rows_R": R, "storage": "fp16 values + 4-bit runs",
@@ -667,11 +795,18 @@ def main() -> int:
         "compressed_bytes_fetched": comp_fetched,
         "pct_peak_hbm_fetched": round(100 * comp_fetched / us_step / 1e3 / PEAK_HBM_GBPS, 2),
         "bytes_requested": total_fetched,
+        "bound_pass_bytes": bound_pass,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
                      "kernel_us": round(us_kernel, 3), "kernel_us_replays": [round(v, 3) for v in samples],
                      "bytes_per_launch": b_alg,
-                     "timing": "HIP events around a graph replay of the K steps on the launch stream"},
+                     "timing": "HIP events around a graph replay of the K steps on the launch stream",
+                     "kernel_trace": None if ktrace is None else {
+                         "mean_us": round(ktrace["mean_ns"] / 1e3, 3), "median_us": round(ktrace["median_ns"] / 1e3, 3),
+                         "frac_mean": round(b_alg / ktrace["mean_ns"] / PEAK_HBM_GBPS, 4),
+                         "frac_median": round(b_alg / ktrace["median_ns"] / PEAK_HBM_GBPS, 4),
+                         "dispatches": ktrace["dispatches"],
+                         "source": os.path.relpath(kernel_trace_file(workload_key), ROOT)}},
         "eager_us_per_call": round(eager_us, 3),
         "launch_floor": {"graph_us": round(floor_kernel, 3), "eager_us": round(floor_wall, 3),
                          "op": "one-element torch fill kernel"},

@@ -9,10 +9,11 @@
  *
  *     y[r] = sum over active k of W[r,k] * x_k,     r = 0 .. M-1,
  *
- * with every product formed exactly in fp32 (Section 5's fp32 arithmetic),
- * summed at least as accurately as fp32 accumulation would (see
- * celty_spmspv), and y rounded to fp16 (round to nearest even).  Inactive
- * columns of W are never read (Section 3.1).
+ * with every product formed exactly in fp32 (two fp16 factors), the products
+ * summed in integer fixed point on grids derived from the magnitudes of the
+ * call's own active columns (celty_spmspv states the arithmetic and its error
+ * bound), and y rounded to fp16 (round to nearest even).  Inactive columns of
+ * W are never read (Section 3.1).
  *
  * General rules
  * -------------
@@ -45,12 +46,15 @@ typedef enum celty_status {
   CELTY_EHIP = 5        /* the HIP runtime reported an error at launch */
 } celty_status;
 
-#define CELTY_FORMAT_VERSION 1
+#define CELTY_FORMAT_VERSION 2
 #define CELTY_RUN_BITS 4   /* 4-bit run lengths (Section 3.2) */
 #define CELTY_GROUP 8      /* entries per aligned group: one 16-byte fp16 vector */
 
+/* Layouts of the per-entry row information (the `layout` field). */
+#define CELTY_LAYOUT_RLC 0 /* 4-bit run lengths, Section 3.2 (the format below) */
+
 /*
- * Tiled RLC-CSC, format version 1 (Section 3.2 plus the readings below).
+ * Tiled RLC-CSC, format version 2 (Section 3.2 plus the readings below).
  *
  * Rows are cut into T = ceil(M/R) tiles of R rows.  Segment (t, k) holds the
  * stored entries of column k inside tile t; segments are laid out tile-major,
@@ -67,9 +71,12 @@ typedef enum celty_status {
  *  - values[8g + j] is the fp16 bit pattern of entry j of group g; runs[g]
  *    holds entry j's run in bits [4j, 4j+4).
  *  - gptr[s] is the first group of segment s; gptr[T*K] = n_groups.
- * The descriptor is plain data; the three arrays are owned by the caller and
- * are host pointers for the encoder/decoder and device pointers for
- * celty_spmspv*.
+ *  - colmax[k] is the fp16 bit pattern of the largest |stored value| of
+ *    column k (+0 when the column stores nothing).  It is not part of the
+ *    paper's format: the product derives its fixed-point scales from it.
+ * Version 1 was the same format without colmax.  The descriptor is plain
+ * data; the arrays are owned by the caller and are host pointers for the
+ * encoder/decoder and device pointers for celty_spmspv*.
  */
 typedef struct celty_rlc_csc {
   int32_t version;          /* CELTY_FORMAT_VERSION */
@@ -79,11 +86,12 @@ typedef struct celty_rlc_csc {
   int64_t n_entries;        /* stored values + padding entries (alignment excluded) */
   int64_t n_nnz;            /* stored values */
   int64_t n_pad;            /* padding entries */
-  float max_abs;            /* largest |stored value| (0 if none); finite */
-  int32_t reserved;         /* 0 */
+  float max_abs;            /* largest |stored value| (0 if none) = the largest colmax; finite */
+  int32_t layout;           /* CELTY_LAYOUT_RLC */
   const uint32_t* gptr;     /* [T*K + 1], 4-byte aligned */
   const uint16_t* values;   /* [8*G] fp16 bits, 16-byte aligned */
   const uint32_t* runs;     /* [G], 4-byte aligned */
+  const uint16_t* colmax;   /* [K] fp16 bits, 4-byte aligned */
 } celty_rlc_csc;
 
 /*
@@ -93,36 +101,38 @@ typedef struct celty_rlc_csc {
  *   mask   host, uint8 row-major with row stride ldm >= K; non-zero = kept.
  *          NULL keeps every entry (then only +-0 weights are dropped).
  *   R      tile height, 1 <= R; T = ceil(M/R).
+ *   layout CELTY_LAYOUT_RLC.
  * Outputs (host, may not be NULL): n_groups, n_nnz, n_pad.
- * Errors: EINVAL (null W or output pointer, M/K/R < 1, short stride),
- *         EOVERFLOW (n_groups > UINT32_MAX), ENOMEM.
+ * Errors: EINVAL (null W or output pointer, M/K/R < 1, short stride, unknown
+ *         layout), EOVERFLOW (n_groups > UINT32_MAX), ENOMEM.
  */
 celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm,
-                               int32_t M, int32_t K, int32_t R,
+                               int32_t M, int32_t K, int32_t R, int32_t layout,
                                int64_t* n_groups, int64_t* n_nnz, int64_t* n_pad);
 
 /*
  * Encode into caller buffers (host): gptr [T*K+1], values [8*n_groups]
- * (16-byte aligned), runs [n_groups].  n_groups must equal the plan's value.
- * On success *out is filled (pointers = the three buffers given here, and
- * max_abs = the largest magnitude among the stored values).
- * n_threads: worker threads, 0 = all hardware threads.  The result does not
- * depend on n_threads.
- * Errors: EINVAL (as for the plan, null buffers, misaligned values,
+ * (16-byte aligned), runs [n_groups], colmax [K] (4-byte aligned).
+ * n_groups must equal the plan's value.  On success *out is filled (pointers
+ * = the buffers given here, and max_abs = the largest magnitude among the
+ * stored values).  n_threads: worker threads, 0 = all hardware threads.  The
+ * result does not depend on n_threads.
+ * Errors: EINVAL (as for the plan, null buffers, misaligned values or colmax,
  *         n_groups mismatch, n_threads < 0), EOVERFLOW, ENOMEM.
  */
 celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm,
-                          int32_t M, int32_t K, int32_t R,
-                          uint32_t* gptr, uint16_t* values, uint32_t* runs, int64_t n_groups,
-                          celty_rlc_csc* out, int32_t n_threads);
+                          int32_t M, int32_t K, int32_t R, int32_t layout,
+                          uint32_t* gptr, uint16_t* values, uint32_t* runs, uint16_t* colmax,
+                          int64_t n_groups, celty_rlc_csc* out, int32_t n_threads);
 
 /*
- * Decode a format-v1 stream held in host memory back to dense form (host).
+ * Decode a stream held in host memory back to dense form (host).
  *   W_out    host, M x K fp16 bits, row-major, stride K: stored values, +0 elsewhere.
  *   mask_out host, M x K uint8, stride K: 1 where a value is stored (may be NULL).
  * Errors: EINVAL (null pointers, bad header), EFORMAT (gptr not monotone from
  * 0 to n_groups, a stored value beyond its tile, an alignment entry with a
- * non-zero run, header counts or max_abs that disagree with the stream).
+ * non-zero run, header counts, max_abs or colmax that disagree with the
+ * stream).
  */
 celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out);
 
@@ -179,8 +189,8 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
 
 /*
  * The dual-sparse SpMSpV (Sections 3.1-3.3): y = W x_A.
- *   W          descriptor with DEVICE pointers (format v1, e.g. the encoder's
- *              arrays copied to the device); must be a valid encoder output.
+ *   W          descriptor with DEVICE pointers (e.g. the encoder's arrays
+ *              copied to the device); must be a valid encoder output.
  *   x          device fp16[K]; must be finite (an infinite x_k is outside the
  *              operation's domain and yields unspecified rows).
  *   tau        threshold, as for celty_select.
@@ -188,15 +198,37 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  *              become +0); must not alias x or the workspace.
  *   workspace  device buffer of at least celty_spmspv_workspace_bytes(M,K,R)
  *              bytes, zero-filled before first use (celty_spmspv_workspace_init).
- * One kernel launch: every workgroup selects the active columns of its slice
- * of x, walks their compressed segments for its row tile, forms each fp32
- * product (exact for fp16 factors), accumulates them in LDS in int32 fixed
- * point scaled per workgroup so that no row can overflow (rounding error per
- * row at most n^2 * max|w x| * 2^-32 for n active columns of the slice), and
- * merges the slices of a row tile with one returning 64-bit atomic per row
- * (fixed point at a launch-wide scale, with an arrival count): the slice
- * that arrives last at a row writes y[row] and clears the slot.  W->max_abs
- * must bound every stored |value| (the encoder sets it).
+ * One kernel launch.  The grid is (row tile t) x (column slice c).  Every
+ * workgroup selects the active columns of its slice that store entries in
+ * its tile (A_ct), walks their compressed segments, forms each product
+ * w * x_k exactly in fp32 and adds it into an LDS tile of R int32 rows:
+ *
+ *   B_ct = sum over k in A_ct of colmax[k] * |x_k|      (fp32)
+ *   s_ct = 30 - e(B_ct), where 2^(e-1) <= B_ct < 2^e     (clamped to [-64, 64])
+ *
+ * and each product is rounded to the nearest multiple of 2^-s_ct (ties
+ * upward) before the integer add, so no partial sum can leave int32.  The
+ * slices of a row tile are merged with one returning 64-bit atomic per row
+ * and slice, in int64 fixed point on the launch-wide grid 2^-s_U:
+ *
+ *   U   = sum over every active k of colmax[k] * |x_k|  (fp32, the same
+ *         summation order in every workgroup, so all agree on it)
+ *   s_U = 48 - e(U)                                      (clamped to [-64, 64])
+ *
+ * each slice's partial being rounded onto that grid (ties upward); the slice
+ * that arrives last at a row writes y[row] = fp16(fp32(sum) * 2^-s_U) and
+ * clears the slot.  With one slice the tile goes straight to y.  Error of a
+ * row r before the final fp32 and fp16 roundings, for n_r products in the
+ * row, KC slices and s_ct not clamped:
+ *
+ *   |sum - exact| <= sum over slices of n_rc * B_ct * 2^-30  +  KC * U * 2^-48
+ *                 <= (n_r * 2^-30 + KC * 2^-48) * U,
+ *
+ * where U >= sum over k of |W[r,k] x_k| for every row r.  (fp32 accumulation
+ * in any order has the worst case (n_r - 1) * 2^-24 * sum_k |W[r,k] x_k|.)
+ * colmax must bound every |stored value| of its column (the encoder sets it
+ * exactly): a smaller value can overflow the int32 tile and give wrong rows,
+ * but never an access outside the arrays.
  * Errors: EINVAL (null or misaligned pointers, inconsistent header, NaN tau,
  *         non-finite or negative max_abs, short workspace, more than 63
  *         column slices, cols_per_block above 512 * waves_per_block,

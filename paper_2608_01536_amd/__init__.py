@@ -40,9 +40,10 @@ _share_torch_hip_runtime()
 _lib = ctypes.CDLL(_LIB_PATH)
 
 CELTY_OK, CELTY_EINVAL, CELTY_ENOMEM, CELTY_EOVERFLOW, CELTY_EFORMAT, CELTY_EHIP = range(6)
-FORMAT_VERSION = 1
+FORMAT_VERSION = 2
 RUN_BITS = 4
 GROUP = 8
+LAYOUT_RLC = 0
 
 _p = ctypes.c_void_p
 _i32, _i64, _f32, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
@@ -51,8 +52,8 @@ _i32, _i64, _f32, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c
 class celty_rlc_csc(ctypes.Structure):
     _fields_ = [("version", _i32), ("M", _i32), ("K", _i32), ("R", _i32), ("T", _i32),
                 ("run_bits", _i32), ("n_groups", _i64), ("n_entries", _i64), ("n_nnz", _i64),
-                ("n_pad", _i64), ("max_abs", _f32), ("reserved", _i32), ("gptr", _p), ("values", _p),
-                ("runs", _p)]
+                ("n_pad", _i64), ("max_abs", _f32), ("layout", _i32), ("gptr", _p), ("values", _p),
+                ("runs", _p), ("colmax", _p)]
 
 
 class celty_launch(ctypes.Structure):
@@ -66,9 +67,9 @@ def _sig(name, res, *args):
     return f
 
 
-_encode_plan = _sig("celty_encode_plan", ctypes.c_int, _p, _i64, _p, _i64, _i32, _i32, _i32,
+_encode_plan = _sig("celty_encode_plan", ctypes.c_int, _p, _i64, _p, _i64, _i32, _i32, _i32, _i32,
                     ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.POINTER(_i64))
-_encode = _sig("celty_encode", ctypes.c_int, _p, _i64, _p, _i64, _i32, _i32, _i32, _p, _p, _p, _i64,
+_encode = _sig("celty_encode", ctypes.c_int, _p, _i64, _p, _i64, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _i64,
                ctypes.POINTER(celty_rlc_csc), _i32)
 _decode = _sig("celty_decode", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _p)
 _select = _sig("celty_select", ctypes.c_int, _p, _i32, _f32, _p, _p, _p)
@@ -110,7 +111,10 @@ def _aligned_empty(n: int, dtype, align: int = 64) -> np.ndarray:
 
 
 def _host_matrix(W: np.ndarray, mask):
-    Wb = np.ascontiguousarray(np.asarray(W)).view(np.uint16)
+    Wa = np.asarray(W)
+    if Wa.dtype not in (np.float16, np.uint16):
+        raise ValueError(f"W must hold fp16 values (float16, or their uint16 bit patterns), not {Wa.dtype}")
+    Wb = np.ascontiguousarray(Wa).view(np.uint16)
     if Wb.ndim != 2:
         raise ValueError("W must be 2-D (M x K)")
     if mask is None:
@@ -125,48 +129,52 @@ def _host_matrix(W: np.ndarray, mask):
 # Host encoder / decoder
 # ---------------------------------------------------------------------------
 class HostRlcCsc:
-    """Format-v1 arrays in host memory plus the header."""
+    """The encoded arrays in host memory plus the header."""
 
-    def __init__(self, desc: celty_rlc_csc, gptr: np.ndarray, values: np.ndarray, runs: np.ndarray):
+    def __init__(self, desc: celty_rlc_csc, gptr: np.ndarray, values: np.ndarray, runs: np.ndarray,
+                 colmax: np.ndarray):
         self.M, self.K, self.R, self.T = desc.M, desc.K, desc.R, desc.T
         self.n_groups, self.n_entries = int(desc.n_groups), int(desc.n_entries)
         self.n_nnz, self.n_pad = int(desc.n_nnz), int(desc.n_pad)
         self.max_abs = float(desc.max_abs)
-        self.gptr, self.values, self.runs = gptr, values, runs
+        self.layout = int(desc.layout)
+        self.gptr, self.values, self.runs, self.colmax = gptr, values, runs, colmax
 
     def desc(self) -> celty_rlc_csc:
         return celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
-                             self.n_entries, self.n_nnz, self.n_pad, self.max_abs, 0, self.gptr.ctypes.data,
+                             self.n_entries, self.n_nnz, self.n_pad, self.max_abs, self.layout,
+                             self.gptr.ctypes.data,
                              self.values.ctypes.data if self.values.size else None,
-                             self.runs.ctypes.data if self.runs.size else None)
+                             self.runs.ctypes.data if self.runs.size else None, self.colmax.ctypes.data)
 
     def to_device(self, device=None) -> "DeviceRlcCsc":
         return DeviceRlcCsc(self, device)
 
 
-def celty_encode_plan(W: np.ndarray, mask, R: int) -> Tuple[int, int, int]:
+def celty_encode_plan(W: np.ndarray, mask, R: int, layout: int = LAYOUT_RLC) -> Tuple[int, int, int]:
     Wb, m = _host_matrix(W, mask)
     M, K = Wb.shape
     g, n, p = _i64(), _i64(), _i64()
-    _check(_encode_plan(Wb.ctypes.data, K, None if m is None else m.ctypes.data, K, M, K, int(R),
+    _check(_encode_plan(Wb.ctypes.data, K, None if m is None else m.ctypes.data, K, M, K, int(R), int(layout),
                         ctypes.byref(g), ctypes.byref(n), ctypes.byref(p)), "celty_encode_plan")
     return g.value, n.value, p.value
 
 
-def celty_encode(W: np.ndarray, mask, R: int, n_threads: int = 0) -> HostRlcCsc:
-    """fp16 W (M x K) + keep-mask -> format v1 in fresh host arrays."""
+def celty_encode(W: np.ndarray, mask, R: int, n_threads: int = 0, layout: int = LAYOUT_RLC) -> HostRlcCsc:
+    """fp16 W (M x K) + keep-mask -> the encoded arrays, in fresh host arrays."""
     Wb, m = _host_matrix(W, mask)
     M, K = Wb.shape
-    G, _, _ = celty_encode_plan(Wb, m, R)
+    G, _, _ = celty_encode_plan(Wb, m, R, layout)
     T = -(-M // int(R))
     gptr = _aligned_empty(T * K + 1, np.uint32)
     values = _aligned_empty(GROUP * G, np.uint16)
     runs = _aligned_empty(G, np.uint32)
+    colmax = _aligned_empty(K, np.uint16)
     desc = celty_rlc_csc()
-    _check(_encode(Wb.ctypes.data, K, None if m is None else m.ctypes.data, K, M, K, int(R),
-                   gptr.ctypes.data, values.ctypes.data, runs.ctypes.data, G, ctypes.byref(desc),
-                   int(n_threads)), "celty_encode")
-    return HostRlcCsc(desc, gptr, values, runs)
+    _check(_encode(Wb.ctypes.data, K, None if m is None else m.ctypes.data, K, M, K, int(R), int(layout),
+                   gptr.ctypes.data, values.ctypes.data, runs.ctypes.data, colmax.ctypes.data, G,
+                   ctypes.byref(desc), int(n_threads)), "celty_encode")
+    return HostRlcCsc(desc, gptr, values, runs, colmax)
 
 
 def celty_decode(enc: HostRlcCsc) -> Tuple[np.ndarray, np.ndarray]:
@@ -192,13 +200,15 @@ def _stream_handle(stream) -> Optional[int]:
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _dev_ptr(t, nbytes_each: int, name: str, min_numel: int = 0, device=None) -> int:
+def _dev_ptr(t, nbytes_each: int, name: str, min_numel: int = 0, device=None, dtypes=None) -> int:
     """Device address of t after the checks the C ABI cannot make itself: the
     library takes bare pointers and trusts the sizes (x holds K halves, y M,
     idx K ints), so a short or misplaced tensor is rejected here, before any
     launch, rather than read or written out of bounds on the GPU."""
     if not t.is_cuda or not t.is_contiguous() or t.element_size() != nbytes_each:
         raise ValueError(f"{name} must be a contiguous CUDA tensor of {nbytes_each}-byte elements")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}; expected one of {', '.join(str(d) for d in dtypes)}")
     if t.numel() < min_numel:
         raise ValueError(f"{name} holds {t.numel()} elements, fewer than the {min_numel} the call uses")
     if device is not None and t.device != device:
@@ -206,8 +216,14 @@ def _dev_ptr(t, nbytes_each: int, name: str, min_numel: int = 0, device=None) ->
     return int(t.data_ptr())
 
 
+def _half_dtypes():
+    """Device tensors that may carry fp16 x or y: float16, or int16 bit patterns."""
+    torch = _torch()
+    return (torch.float16, torch.int16)
+
+
 class DeviceRlcCsc:
-    """Format-v1 arrays copied into device tensors, plus a device descriptor."""
+    """The encoded arrays copied into device tensors, plus a device descriptor."""
 
     def __init__(self, host: HostRlcCsc, device=None):
         torch = _torch()
@@ -217,16 +233,21 @@ class DeviceRlcCsc:
         self.n_groups, self.n_entries = host.n_groups, host.n_entries
         self.n_nnz, self.n_pad = host.n_nnz, host.n_pad
         self.max_abs = host.max_abs
+        self.layout = host.layout
         self.gptr = torch.from_numpy(host.gptr.view(np.int32)).to(device)
         # at least one element so that pointers are never null
         self.values = torch.from_numpy(host.values.view(np.int16) if host.values.size
                                        else np.zeros(8, np.int16)).to(device)
         self.runs = torch.from_numpy(host.runs.view(np.int32) if host.runs.size
                                      else np.zeros(1, np.int32)).to(device)
-        self._desc = celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
-                                   self.n_entries, self.n_nnz, self.n_pad, self.max_abs, 0,
-                                   self.gptr.data_ptr(),
-                                   self.values.data_ptr(), self.runs.data_ptr())
+        self.colmax = torch.from_numpy(host.colmax.view(np.int16)).to(device)
+        self._desc = self._make_desc()
+
+    def _make_desc(self) -> celty_rlc_csc:
+        return celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
+                             self.n_entries, self.n_nnz, self.n_pad, self.max_abs, self.layout,
+                             self.gptr.data_ptr(), self.values.data_ptr(), self.runs.data_ptr(),
+                             self.colmax.data_ptr())
 
     def desc(self) -> celty_rlc_csc:
         return self._desc
@@ -236,10 +257,8 @@ class DeviceRlcCsc:
         other = object.__new__(DeviceRlcCsc)
         other.__dict__.update(self.__dict__)
         other.gptr, other.values, other.runs = self.gptr.clone(), self.values.clone(), self.runs.clone()
-        other._desc = celty_rlc_csc(FORMAT_VERSION, self.M, self.K, self.R, self.T, RUN_BITS, self.n_groups,
-                                    self.n_entries, self.n_nnz, self.n_pad, self.max_abs, 0,
-                                    other.gptr.data_ptr(),
-                                    other.values.data_ptr(), other.runs.data_ptr())
+        other.colmax = self.colmax.clone()
+        other._desc = other._make_desc()
         return other
 
 
@@ -261,7 +280,7 @@ def new_workspace(W: DeviceRlcCsc, device=None):
 
 def celty_select(x, tau: float, idx, count, stream=None) -> None:
     K = x.numel()
-    _check(_select(_dev_ptr(x, 2, "x"), K, float(tau), _dev_ptr(idx, 4, "idx", K, x.device),
+    _check(_select(_dev_ptr(x, 2, "x", 0, None, _half_dtypes()), K, float(tau), _dev_ptr(idx, 4, "idx", K, x.device),
                    _dev_ptr(count, 4, "count", 1, x.device), _stream_handle(stream)), "celty_select")
 
 
@@ -277,7 +296,8 @@ def _launch_struct(launch) -> Optional[celty_launch]:
 
 def celty_spmspv(W: DeviceRlcCsc, x, tau: float, y, workspace, stream=None) -> None:
     d, dev = W.desc(), W.gptr.device
-    _check(_spmspv(ctypes.byref(d), _dev_ptr(x, 2, "x", W.K, dev), float(tau), _dev_ptr(y, 2, "y", W.M, dev),
+    hd = _half_dtypes()
+    _check(_spmspv(ctypes.byref(d), _dev_ptr(x, 2, "x", W.K, dev, hd), float(tau), _dev_ptr(y, 2, "y", W.M, dev, hd),
                    _dev_ptr(workspace, 1, "workspace", 0, dev), workspace.numel(), _stream_handle(stream)),
            "celty_spmspv")
 
@@ -285,7 +305,8 @@ def celty_spmspv(W: DeviceRlcCsc, x, tau: float, y, workspace, stream=None) -> N
 def celty_spmspv_ex(W: DeviceRlcCsc, x, tau: float, y, workspace, launch=None, stream=None) -> None:
     d, dev = W.desc(), W.gptr.device
     ls = _launch_struct(launch)
-    _check(_spmspv_ex(ctypes.byref(d), _dev_ptr(x, 2, "x", W.K, dev), float(tau), _dev_ptr(y, 2, "y", W.M, dev),
+    hd = _half_dtypes()
+    _check(_spmspv_ex(ctypes.byref(d), _dev_ptr(x, 2, "x", W.K, dev, hd), float(tau), _dev_ptr(y, 2, "y", W.M, dev, hd),
                       _dev_ptr(workspace, 1, "workspace", 0, dev), workspace.numel(),
                       None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_ex")
 
@@ -314,8 +335,9 @@ def celty_spmspv_batch(Ws, xs, taus, ys, workspace, launch=None, stream=None) ->
     if not (len(xs) == len(taus) == len(ys) == n):
         raise ValueError("Ws, xs, taus and ys must have the same length")
     descs, arr = _desc_array(Ws)
-    xp = (_p * n)(*[_dev_ptr(x, 2, f"xs[{i}]", W.K, W.gptr.device) for i, (W, x) in enumerate(zip(Ws, xs))])
-    yp = (_p * n)(*[_dev_ptr(y, 2, f"ys[{i}]", W.M, W.gptr.device) for i, (W, y) in enumerate(zip(Ws, ys))])
+    hd = _half_dtypes()
+    xp = (_p * n)(*[_dev_ptr(x, 2, f"xs[{i}]", W.K, W.gptr.device, hd) for i, (W, x) in enumerate(zip(Ws, xs))])
+    yp = (_p * n)(*[_dev_ptr(y, 2, f"ys[{i}]", W.M, W.gptr.device, hd) for i, (W, y) in enumerate(zip(Ws, ys))])
     tp = (_f32 * n)(*[float(t) for t in taus])
     ls = _launch_struct(launch)
     dev = Ws[0].gptr.device if n else None
@@ -339,7 +361,7 @@ def default_tile_rows(M: int, K: int) -> int:
 
 
 __all__ = [
-    "default_tile_rows",
+    "FORMAT_VERSION", "LAYOUT_RLC", "default_tile_rows",
     "celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv", "celty_spmspv_ex",
     "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "new_batch_workspace",
     "celty_spmspv_plan", "celty_spmspv_workspace_bytes", "celty_spmspv_workspace_init", "celty_status_string",

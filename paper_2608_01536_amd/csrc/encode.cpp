@@ -113,19 +113,20 @@ void count_item(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm
 }
 
 celty_status check_common(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm,
-                          int32_t M, int32_t K, int32_t R) {
+                          int32_t M, int32_t K, int32_t R, int32_t layout) {
   if (!W || M < 1 || K < 1 || R < 1 || ldw < K) return CELTY_EINVAL;
   if (mask && ldm < K) return CELTY_EINVAL;
+  if (layout != CELTY_LAYOUT_RLC) return CELTY_EINVAL;
   return CELTY_OK;
 }
 
 }  // namespace
 
 extern "C" celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const uint8_t* mask,
-                                          int64_t ldm, int32_t M, int32_t K, int32_t R,
+                                          int64_t ldm, int32_t M, int32_t K, int32_t R, int32_t layout,
                                           int64_t* n_groups, int64_t* n_nnz, int64_t* n_pad) {
   if (!n_groups || !n_nnz || !n_pad) return CELTY_EINVAL;
-  if (celty_status st = check_common(W, ldw, mask, ldm, M, K, R)) return st;
+  if (celty_status st = check_common(W, ldw, mask, ldm, M, K, R, layout)) return st;
   try {
     const int32_t T = int32_t((int64_t(M) + R - 1) / R);
     const std::vector<Item> items = make_items(T, K);
@@ -159,14 +160,14 @@ extern "C" celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const 
 }
 
 extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8_t* mask,
-                                     int64_t ldm, int32_t M, int32_t K, int32_t R, uint32_t* gptr,
-                                     uint16_t* values, uint32_t* runs, int64_t n_groups,
-                                     celty_rlc_csc* out, int32_t n_threads) {
-  if (celty_status st = check_common(W, ldw, mask, ldm, M, K, R)) return st;
-  if (!gptr || !out || n_threads < 0 || n_groups < 0) return CELTY_EINVAL;
+                                     int64_t ldm, int32_t M, int32_t K, int32_t R, int32_t layout,
+                                     uint32_t* gptr, uint16_t* values, uint32_t* runs, uint16_t* colmax,
+                                     int64_t n_groups, celty_rlc_csc* out, int32_t n_threads) {
+  if (celty_status st = check_common(W, ldw, mask, ldm, M, K, R, layout)) return st;
+  if (!gptr || !out || !colmax || n_threads < 0 || n_groups < 0) return CELTY_EINVAL;
   if (n_groups > 0 && (!values || !runs)) return CELTY_EINVAL;
   if ((reinterpret_cast<uintptr_t>(values) & 15u) || (reinterpret_cast<uintptr_t>(runs) & 3u) ||
-      (reinterpret_cast<uintptr_t>(gptr) & 3u))
+      (reinterpret_cast<uintptr_t>(gptr) & 3u) || (reinterpret_cast<uintptr_t>(colmax) & 3u))
     return CELTY_EINVAL;
   if (n_groups > int64_t(UINT32_MAX)) return CELTY_EOVERFLOW;
   try {
@@ -174,7 +175,9 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
     const int64_t nseg = int64_t(T) * K;
     const std::vector<Item> items = make_items(T, K);
     std::vector<int64_t> nnz(items.size()), pad(items.size());
-    std::vector<uint16_t> vmax(items.size(), 0);   // largest |value| bits per item
+    // largest |value| bits of column k within tile t, at t*K + k (each item
+    // writes only its own columns of its own tile)
+    std::vector<uint16_t> tile_colmax(size_t(nseg), 0);
 
     // pass 1: groups per segment, written into gptr[s] (then scanned in place)
     bool ok = parallel_items(items.size(), n_threads, [&](size_t i) {
@@ -225,7 +228,8 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
           }
           const uint16_t v = W[r * ldw + it.k0 + j];
           emit(j, v, uint32_t(gap));
-          vmax[i] = std::max<uint16_t>(vmax[i], uint16_t(v & 0x7FFFu));
+          uint16_t& cm = tile_colmax[size_t(sbase + j)];
+          cm = std::max<uint16_t>(cm, uint16_t(v & 0x7FFFu));   // magnitude bits order like the values
           last[j] = rel;
         }
       }
@@ -234,11 +238,16 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
     if (!ok) return CELTY_ENOMEM;
 
     int64_t A = 0, B = 0;
-    uint16_t mbits = 0;
     for (size_t i = 0; i < items.size(); ++i) {
       A += nnz[i];
       B += pad[i];
-      mbits = std::max(mbits, vmax[i]);   // magnitude bits order like the values
+    }
+    uint16_t mbits = 0;
+    for (int32_t k = 0; k < K; ++k) {
+      uint16_t m = 0;
+      for (int32_t t = 0; t < T; ++t) m = std::max(m, tile_colmax[size_t(t) * K + k]);
+      colmax[k] = m;
+      mbits = std::max(mbits, m);
     }
     out->version = CELTY_FORMAT_VERSION;
     out->M = M;
@@ -251,10 +260,11 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
     out->n_nnz = A;
     out->n_pad = B;
     out->max_abs = half_bits_to_float(mbits);
-    out->reserved = 0;
+    out->layout = layout;
     out->gptr = gptr;
     out->values = values;
     out->runs = runs;
+    out->colmax = colmax;
     return CELTY_OK;
   } catch (...) {
     return CELTY_ENOMEM;
@@ -264,10 +274,11 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
 extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out) {
   if (!enc || !W_out) return CELTY_EINVAL;
   if (enc->version != CELTY_FORMAT_VERSION || enc->run_bits != CELTY_RUN_BITS) return CELTY_EINVAL;
+  if (enc->layout != CELTY_LAYOUT_RLC) return CELTY_EINVAL;
   const int32_t M = enc->M, K = enc->K, R = enc->R, T = enc->T;
   if (M < 1 || K < 1 || R < 1 || T != int32_t((int64_t(M) + R - 1) / R) || enc->n_groups < 0)
     return CELTY_EINVAL;
-  if (!enc->gptr || (enc->n_groups > 0 && (!enc->values || !enc->runs))) return CELTY_EINVAL;
+  if (!enc->gptr || !enc->colmax || (enc->n_groups > 0 && (!enc->values || !enc->runs))) return CELTY_EINVAL;
   const int64_t nseg = int64_t(T) * K;
   const uint32_t* gptr = enc->gptr;
   if (gptr[0] != 0 || int64_t(gptr[nseg]) != enc->n_groups) return CELTY_EFORMAT;
@@ -277,6 +288,12 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
   if (mask_out) std::memset(mask_out, 0, size_t(M) * K);
   int64_t nnz = 0, pad = 0;
   uint16_t mbits = 0;
+  std::vector<uint16_t> cmax;
+  try {
+    cmax.assign(size_t(K), 0);
+  } catch (...) {
+    return CELTY_ENOMEM;
+  }
   for (int64_t s = 0; s < nseg; ++s) {
     const int64_t t = s / K, k = s % K;
     const int64_t hi = std::min<int64_t>(M, (t + 1) * int64_t(R));
@@ -298,6 +315,7 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
         W_out[row * K + k] = v;
         if (mask_out) mask_out[row * K + k] = 1;
         mbits = std::max<uint16_t>(mbits, uint16_t(v & 0x7FFFu));
+        cmax[size_t(k)] = std::max<uint16_t>(cmax[size_t(k)], uint16_t(v & 0x7FFFu));
         ++nnz;
       } else {
         ++pad;
@@ -306,5 +324,7 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
   }
   if (nnz != enc->n_nnz || pad != enc->n_pad || nnz + pad != enc->n_entries) return CELTY_EFORMAT;
   if (enc->max_abs != half_bits_to_float(mbits)) return CELTY_EFORMAT;
+  for (int32_t k = 0; k < K; ++k)
+    if (enc->colmax[k] != cmax[size_t(k)]) return CELTY_EFORMAT;
   return CELTY_OK;
 }

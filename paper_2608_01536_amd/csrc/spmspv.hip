@@ -20,15 +20,18 @@
 //   * each product value * x_k is exact in fp32 (two fp16 factors) and is
 //     added into an LDS tile of the R output rows (Section 3.3's
 //     scatter-accumulation in on-chip memory).  The tile holds int32 fixed
-//     point with a per-workgroup power-of-two scale 2^s chosen so that no row
-//     of the slice can overflow: on gfx950 an LDS integer atomic add costs a
-//     small fraction of an fp32 one, and the rounding error of a row,
-//     n^2 * max|w x| * 2^-32 for n active columns in the slice, stays below
-//     the worst case of fp32 accumulation;
+//     point on a per-workgroup grid 2^-s derived from the slice's own data:
+//     B = sum over its kept columns of colmax[k] * |x_k| bounds every row's
+//     sum of |products|, and 2^s puts B just below 2^30, so no row can
+//     overflow (on gfx950 an LDS integer atomic add costs a small fraction of
+//     an fp32 one);
 //   * the slices of a row tile are merged with one returning 64-bit atomic
-//     per row (fixed point at a launch-wide scale plus an arrival count); the
-//     slice that arrives last writes y[row] in fp16 and clears the slot for
-//     the next call.  With a single slice the tile goes straight to y.
+//     per row: fixed point on a launch-wide grid plus an arrival count.  The
+//     grid comes from U = sum over every active column of colmax[k] * |x_k|,
+//     which every workgroup sums from x and colmax in the same order (so all
+//     agree on it) while its first compressed loads are in flight.  The slice
+//     that arrives last writes y[row] in fp16 and clears the slot for the
+//     next call.  With a single slice the tile goes straight to y.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -63,17 +66,6 @@ __device__ __forceinline__ unsigned short float_to_half_bits(float v) {
   return __half_as_ushort(__float2half_rn(v));
 }
 
-// The same pattern with max: lane 63 ends with the wavefront maximum.
-__device__ __forceinline__ uint32_t wave_inclusive_max(uint32_t v) {
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x142, 0xA, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x143, 0xC, 0xF, false)));
-  return v;
-}
-
 // Orders LDS writes of some lanes before LDS reads of other lanes of the
 // same wavefront.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -82,7 +74,7 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Inclusive scan / suffix minimum over the 16 lanes of each DPP row.
+// Inclusive scan over the 16 lanes of each DPP row.
 __device__ __forceinline__ uint32_t row_inclusive_scan(uint32_t v) {
   v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false));
   v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false));
@@ -90,57 +82,142 @@ __device__ __forceinline__ uint32_t row_inclusive_scan(uint32_t v) {
   v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false));
   return v;
 }
-__device__ __forceinline__ uint32_t row_inclusive_max(uint32_t v) {
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false)));
-  return v;
+
+// Sum over the 64 lanes (every lane gets it): DPP row shifts and broadcasts
+// in a fixed order, so the same inputs give the same bits in every wavefront.
+__device__ __forceinline__ float wave_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x111, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x112, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x114, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x118, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), kWave - 1));
 }
 
-// Block-wide: exclusive scans of a and b, their totals, and the maximum of m
-// (WAVES <= 16).  Each wavefront's totals go to part[] (3*WAVES words, used
-// once per launch); after the barrier lane l < WAVES of every wavefront reads
-// wavefront l's totals and one row scan gives the offsets of all wavefronts.
+// Block-wide: exclusive scans of a and b, their totals, and the sum of the
+// non-negative floats f (WAVES <= 16).  Each wavefront's totals go to part[]
+// (3*WAVES words, used once per launch); after the barrier lane l < WAVES of
+// every wavefront reads wavefront l's totals and one row scan gives the
+// offsets of all wavefronts.
 template <int WAVES>
-__device__ __forceinline__ void block_scan_select(uint32_t a, uint32_t b, uint32_t m, uint32_t& ea, uint32_t& eb,
-                                                  uint32_t& ta, uint32_t& tb, uint32_t& tm, uint32_t* part) {
+__device__ __forceinline__ void block_scan_select(uint32_t a, uint32_t b, float f, uint32_t& ea, uint32_t& eb,
+                                                  uint32_t& ta, uint32_t& tb, float& tf, uint32_t* part) {
   static_assert(WAVES <= 16, "one DPP row holds the per-wavefront totals");
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
   const uint32_t ia = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(a)));
   const uint32_t ib = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(b)));
-  const uint32_t im = wave_inclusive_max(m);
+  const float sf = wave_sum(f);
   if (lane == kWave - 1) {
     part[wv] = ia;
     part[WAVES + wv] = ib;
-    part[2 * WAVES + wv] = im;
+    part[2 * WAVES + wv] = __float_as_uint(sf);
   }
   __syncthreads();
-  uint32_t pa = 0, pb = 0, pm = 0;
+  uint32_t pa = 0, pb = 0;
+  float pf = 0.f;
   if (lane < WAVES) {
     pa = part[lane];
     pb = part[WAVES + lane];
-    pm = part[2 * WAVES + lane];
+    pf = __uint_as_float(part[2 * WAVES + lane]);
   }
-  const uint32_t sa = row_inclusive_scan(pa), sb = row_inclusive_scan(pb), sm = row_inclusive_max(pm);
+  const uint32_t sa = row_inclusive_scan(pa), sb = row_inclusive_scan(pb);
   ta = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sa), WAVES - 1));
   tb = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sb), WAVES - 1));
-  tm = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sm), WAVES - 1));
+  tf = 0.f;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) tf += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pf), w));
   const uint32_t oa = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sa - pa), wv));
   const uint32_t ob = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sb - pb), wv));
   ea = oa + ia - a;
   eb = ob + ib - b;
 }
 
-// Fixed-point scale of a slice: a row sums at most n_seg terms, each at most
-// max|w| * max|x| in magnitude; 2^s puts that bound at or below 2^30.
-__device__ __forceinline__ int fixed_point_scale(uint32_t n_seg, float max_abs, uint32_t xmax_bits) {
-  const float bound = static_cast<float>(n_seg) * max_abs * __uint_as_float(xmax_bits);
-  if (!(bound > 0.f)) return 0;
-  int e;
-  frexpf(bound, &e);   // bound < 2^e
-  return min(max(30 - e, -64), 64);
+// The grid 2^-s whose scale puts a bound b just below 2^top: with
+// 2^(e-1) <= b < 2^e, s = top - e (clamped to [-64, 64]; 0 for b = 0; the
+// exponent of a non-finite b reads as 0).
+__device__ __forceinline__ int grid_scale(float b, int top) {
+  if (!(b > 0.f)) return 0;
+  return min(max(top - __builtin_amdgcn_frexp_expf(b), -64), 64);
+}
+
+// |x| * m for the fp16 halves x and m of two words (the product of two fp16
+// values is exact in fp32), or 0 unless |x| > tau (a NaN x fails the test).
+__device__ __forceinline__ float bound_term(uint32_t xbits, uint32_t mbits, float tau) {
+  const float ax = fabsf(half_bits_to_float(xbits & 0xFFFFu));
+  return ax > tau ? ax * half_bits_to_float(mbits & 0xFFFFu) : 0.f;
+}
+
+// The launch-wide bound U = sum over the active columns k < K of
+// colmax[k] * |x_k|.  Every workgroup sums the same terms in the same order:
+// lane tid of the workgroup takes the column pairs (2d, 2d+1) for
+// d = tid + j * NT (two fp16 per 32-bit load, from x and from colmax), then
+// the wavefronts' sums are added in wavefront order.  The loads of up to
+// kBoundPairs pairs per lane are issued first (issue) and summed later
+// (partial), so that they can overlap other memory traffic; pairs beyond
+// that, an odd last column and an x that is only 2-byte aligned are loaded
+// and summed in partial itself.
+constexpr int kBoundPairs = 16;
+struct BoundLoads {
+  uint32_t xw[kBoundPairs], mw[kBoundPairs];
+};
+
+__device__ __forceinline__ bool bound_fast(const unsigned short* x) {
+  return (reinterpret_cast<uintptr_t>(x) & 3u) == 0;
+}
+
+template <int NT>
+__device__ __forceinline__ void bound_issue(BoundLoads& bl, const unsigned short* x, const unsigned short* colmax,
+                                            int K) {
+  const int pairs = K >> 1;
+  if (!bound_fast(x) || pairs == 0) return;   // workgroup-uniform
+  const auto xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned short*>(x), static_cast<short>(0), 4 * pairs,
+                                                    0x00020000);
+  const auto mr = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned short*>(colmax), static_cast<short>(0),
+                                                    4 * pairs, 0x00020000);
+  const int nj = min((pairs + NT - 1) / NT, kBoundPairs);
+#pragma unroll
+  for (int j = 0; j < kBoundPairs; ++j) {
+    bl.xw[j] = bl.mw[j] = 0u;
+    if (j < nj) {   // workgroup-uniform; pairs past the end read as zero
+      const int off = 4 * (static_cast<int>(threadIdx.x) + j * NT);
+      bl.xw[j] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0);
+      bl.mw[j] = __builtin_amdgcn_raw_buffer_load_b32(mr, off, 0, 0);
+    }
+  }
+}
+
+// This lane's part of U (see bound_issue), summed over the wavefront.
+template <int NT>
+__device__ __forceinline__ float bound_partial(const BoundLoads& bl, const unsigned short* x,
+                                               const unsigned short* colmax, int K, float tau) {
+  float acc = 0.f;
+  const int tid = static_cast<int>(threadIdx.x);
+  if (bound_fast(x)) {
+    const int pairs = K >> 1;
+    const int nj = (pairs + NT - 1) / NT;
+#pragma unroll
+    for (int j = 0; j < kBoundPairs; ++j) {
+      if (j < nj) {
+        acc += bound_term(bl.xw[j], bl.mw[j], tau);
+        acc += bound_term(bl.xw[j] >> 16, bl.mw[j] >> 16, tau);
+      }
+    }
+    for (int j = kBoundPairs; j < nj; ++j) {
+      const int d = tid + j * NT;
+      if (d < pairs) {
+        const uint32_t xw = reinterpret_cast<const uint32_t*>(x)[d];
+        const uint32_t mw = reinterpret_cast<const uint32_t*>(colmax)[d];
+        acc += bound_term(xw, mw, tau);
+        acc += bound_term(xw >> 16, mw >> 16, tau);
+      }
+    }
+    if ((K & 1) && tid == 0) acc += bound_term(x[K - 1], colmax[K - 1], tau);
+  } else {
+    for (int k = tid; k < K; k += NT) acc += bound_term(x[k], colmax[k], tau);
+  }
+  return wave_sum(acc);
 }
 
 // Start of wavefront w's range of the slice's n_grp groups.  A SIMD holds
@@ -417,9 +494,8 @@ struct KernelArgs {
   const unsigned short* x;      // fp16 bits
   unsigned short* y;            // fp16 bits
   unsigned long long* ws;       // [M] merge tickets (see the merge below)
+  const unsigned short* colmax; // [K] fp16 bits: largest |stored weight| of each column
   float tau;
-  float max_abs;                // max |stored weight|
-  int s_glob;                   // fixed-point scale of the cross-slice merge
   uint32_t n_groups;
   int M, K, R, Kc, KC, tile_slots;
   int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS (the tile is at 0)
@@ -436,7 +512,7 @@ struct BatchArgs {
 };
 
 // The arguments a workgroup's prologue needs (the selection's pointers and
-// sizes, the LDS layout, max|w|, R and M).  A single-product launch passes
+// sizes, the LDS layout, the column maxima, R and M).  A single-product launch passes
 // them as leading kernel arguments, which gfx950 preloads into scalar
 // registers at dispatch (the library is built with
 // -amdgpu-kernarg-preload-count), so neither the selection's first memory
@@ -447,7 +523,7 @@ struct Early {
   int K, Kc, KC;
   float tau;
   int tile_slots, seg_off, scr_off, misc_off;   // LDS layout
-  float max_abs;
+  const unsigned short* colmax;
   int R, M;
 };
 
@@ -462,7 +538,8 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem));
   SegInfo* seg = reinterpret_cast<SegInfo*>(smem + e.seg_off);
   int* scr_all = reinterpret_cast<int*>(smem + e.scr_off);
-  uint32_t* part = reinterpret_cast<uint32_t*>(smem + e.misc_off);   // 3*WAVES
+  uint32_t* part = reinterpret_cast<uint32_t*>(smem + e.misc_off);   // 3*WAVES: the selection's scan
+  float* part_u = reinterpret_cast<float*>(smem + e.misc_off) + 3 * WAVES;   // WAVES: sums of U
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int t = blk / e.KC, c = blk - t * e.KC;
@@ -474,14 +551,15 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   const int kn = min(e.Kc, e.K - k0);
   const uint32_t* gp = e.gptr + static_cast<size_t>(t) * e.K + k0;
   const bool one_per_lane = kn <= NT;   // workgroup-uniform
-  uint32_t g[kMaxCols + 1], xr[kMaxCols];
+  uint32_t g[kMaxCols + 1], xr[kMaxCols], cm[kMaxCols];
   int m = 1, kb = tid;
   if (one_per_lane) {
-    g[0] = g[1] = xr[0] = 0u;
+    g[0] = g[1] = xr[0] = cm[0] = 0u;
     if (tid < kn) {
       g[0] = gp[tid];
       g[1] = gp[tid + 1];
       xr[0] = e.x[k0 + tid];
+      cm[0] = e.colmax[k0 + tid];
     }
   } else {
     // m <= kMaxCols consecutive columns per lane; all kMaxCols slots are
@@ -494,6 +572,8 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     for (int j = 0; j <= kMaxCols; ++j) g[j] = gp[min(kb + j, kn)];
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) xr[j] = e.x[k0 + min(kb + j, kn - 1)];
+#pragma unroll
+    for (int j = 0; j < kMaxCols; ++j) cm[j] = e.colmax[k0 + min(kb + j, kn - 1)];
   }
 
   const int row0 = t * e.R;
@@ -507,6 +587,10 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // ---- selection of this slice's active, non-empty columns ----------------
   // The flat group sequence is then cut into equal ranges, one per
   // wavefront (a segment may be shared by several).
+  // B = sum over the kept columns of colmax[k] * |x_k| bounds the sum of
+  // |products| of every row of the slice; the tile's grid 2^-scale puts B
+  // just below 2^30 (float rounding of B and the products' half-unit
+  // roundings stay far inside int32)
   uint32_t n_seg, n_grp;
   if (one_per_lane) {
     // one column per lane
@@ -514,17 +598,18 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     const float xv = half_bits_to_float(xr[0]);
     const bool keep = tid < kn && fabsf(xv) > e.tau && g1 > g0;
     const uint32_t cnt = keep ? g1 - g0 : 0u;
-    // |x| >= 0 orders like its bit pattern
-    uint32_t en, eg, xmax_bits;
-    block_scan_select<WAVES>(keep ? 1u : 0u, cnt, keep ? __float_as_uint(fabsf(xv)) : 0u, en, eg, n_seg, n_grp,
-                             xmax_bits, part);
-    const int s = fixed_point_scale(n_seg, e.max_abs, xmax_bits);
+    uint32_t en, eg;
+    float bound;
+    block_scan_select<WAVES>(keep ? 1u : 0u, cnt, keep ? fabsf(xv) * half_bits_to_float(cm[0]) : 0.f, en, eg,
+                             n_seg, n_grp, bound, part);
+    const int s = grid_scale(bound, 30);
     if (keep) seg[en] = SegInfo{g0, eg, cnt, ldexpf(xv, s)};
     scale = s;
   } else {
     // m <= kMaxCols consecutive columns per lane (loaded above), so one block
     // scan still orders all of them: segment order is column order
-    uint32_t keep_bits = 0u, n_loc = 0u, g_loc = 0u, m_loc = 0u;
+    uint32_t keep_bits = 0u, n_loc = 0u, g_loc = 0u;
+    float b_loc = 0.f;
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) {
       const float xv = half_bits_to_float(xr[j]);
@@ -532,11 +617,12 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
       keep_bits |= (keep ? 1u : 0u) << j;
       n_loc += keep ? 1u : 0u;
       g_loc += keep ? g[j + 1] - g[j] : 0u;
-      m_loc = max(m_loc, keep ? __float_as_uint(fabsf(xv)) : 0u);
+      b_loc += keep ? fabsf(xv) * half_bits_to_float(cm[j]) : 0.f;
     }
-    uint32_t en, eg, xmax_bits;
-    block_scan_select<WAVES>(n_loc, g_loc, m_loc, en, eg, n_seg, n_grp, xmax_bits, part);
-    const int s = fixed_point_scale(n_seg, e.max_abs, xmax_bits);
+    uint32_t en, eg;
+    float bound;
+    block_scan_select<WAVES>(n_loc, g_loc, b_loc, en, eg, n_seg, n_grp, bound, part);
+    const int s = grid_scale(bound, 30);
     uint32_t idx = en, off = eg;
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) {
@@ -564,19 +650,30 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   const int wvu = __builtin_amdgcn_readfirstlane(wv);
   const uint32_t pb0 = cut_of<WAVES>(wvu, n_grp);
   const uint32_t pe = cut_of<WAVES>(wvu + 1, n_grp);
-  if (pb0 < pe) {
-    SegInfo s0;
-    const int i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
-    const int i_end = static_cast<int>(n_seg);
-    const Streams st = make_streams(p.values, p.runs, p.n_groups);
-    int* scr = scr_all + wv * kWave * G;
-    const int n_pass = static_cast<int>((pe - pb0 + P - 1) / P);
+  // The merge's bound U (several slices only): its loads go out before the
+  // ring's, and it is summed while the ring's first passes are in flight.
+  const bool merged = e.KC > 1;   // workgroup-uniform
+  BoundLoads bl;
+  if (merged) bound_issue<NT>(bl, e.x, e.colmax, e.K);
+  const bool has_work = pb0 < pe;   // wavefront-uniform
+  SegInfo s0{0u, 0u, 0u, 0.f};
+  int i_begin = 0;
+  const int i_end = static_cast<int>(n_seg);
+  const Streams st = make_streams(p.values, p.runs, p.n_groups);
+  int* scr = scr_all + wv * kWave * G;
+  const int n_pass = has_work ? static_cast<int>((pe - pb0 + P - 1) / P) : 0;
+  uint32_t before = 0u;
+  uint32_t rb[4] = {0u, 0u, 0u, 0u};
+  Pass<G> ring[DEPTH];
+  uint32_t pf = pb0;    // flat start of the next pass to fetch
+  int icur = 0;         // segment holding group pf
+  if (has_work) {
+    i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
     // A range that starts inside a segment starts at the row reached by the
     // segment's earlier groups: their runs (up to 4 * 64 groups here, the
     // rest below) are loaded ahead of the ring, so that their round trip
     // overlaps the ring's.
-    const uint32_t before = pb0 - s0.off;
-    uint32_t rb[4] = {0u, 0u, 0u, 0u};
+    before = pb0 - s0.off;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (before > static_cast<uint32_t>(q * kWave)) {   // wavefront-uniform
@@ -586,15 +683,19 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
         rb[q] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + j) << 2), 0, 0);
       }
     }
-    Pass<G> ring[DEPTH];
-    uint32_t pf = pb0;    // flat start of the next pass to fetch
-    int icur = i_begin;   // segment holding group pf
+    icur = i_begin;
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) {
       fetch_pass<G>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
       icur = next_pass_segment<G>(ring[d], pf, i_end);
       pf += P;
     }
+  }
+  if (merged) {
+    const float u = bound_partial<NT>(bl, e.x, e.colmax, e.K, e.tau);
+    if (lane == 0) part_u[wv] = u;
+  }
+  if (has_work) {
     uint32_t pb = pb0;    // flat start of the pass being accumulated
     int carry = 0;        // 4 * sum of (run + 1) over its first segment's earlier groups
     if (before > 0u) {
@@ -625,23 +726,30 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   __syncthreads();
 
   // ---- merge --------------------------------------------------------------
-  if (e.KC == 1) {
+  if (!merged) {
     for (int r = tid; r < rows; r += NT)
       p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -scale));
     return;
   }
   // Every slice adds one ticket per row with a returning 64-bit atomic: its
-  // partial sum as fixed point at the launch-wide scale 2^s_glob (|v| <= 2^48
-  // by the choice of s_glob) plus a bias of 2^49 that keeps each ticket
-  // positive, and 1 in the count byte (bits 56..63).  The slice whose atomic
-  // returns count KC-1 is the last for that row: old + its ticket is the
-  // complete sum, so it writes y and clears the slot for the next call.
-  // KC <= 63 keeps the biased sum below 2^56.
+  // partial sum as fixed point on the launch-wide grid 2^-s_glob plus a bias
+  // of 2^49 that keeps each ticket positive, and 1 in the count byte (bits
+  // 56..63).  s_glob puts U, which bounds every slice's partial and their
+  // sum, just below 2^48.  The slice whose atomic returns count KC-1 is the
+  // last for that row: old + its ticket is the complete sum, so it writes y
+  // and clears the slot for the next call.  KC <= 63 keeps the biased sum
+  // below 2^56.
+  float u_total = 0.f;   // the wavefronts' sums in wavefront order: the same bits in every workgroup
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) u_total += part_u[w];
+  const int s_glob = grid_scale(u_total, 48);
   constexpr long long kBias = 1ll << 49;
   constexpr unsigned long long kCount = 1ull << 56;
-  const int shift = p.s_glob - scale;
+  const int shift = s_glob - scale;
   const auto fixed_at_launch_scale = [&](long long q) -> long long {
-    if (shift >= 0) return q * (1ll << shift);
+    // a valid colmax keeps B within a rounding of U, so shift <= 19; the
+    // clamp only keeps a wrong one from an undefined shift
+    if (shift >= 0) return q * (1ll << min(shift, 30));
     const int rs = -shift;   // round half up onto the coarser grid
     return rs > 62 ? 0 : ((q + (1ll << (rs - 1))) >> rs);
   };
@@ -649,7 +757,7 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     if ((old >> 56) == static_cast<unsigned long long>(e.KC - 1)) {
       const long long total = static_cast<long long>((old & (kCount - 1)) + (ticket & (kCount - 1))) -
                               static_cast<long long>(e.KC) * kBias;
-      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(total), -p.s_glob));
+      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(total), -s_glob));
       p.ws[row0 + r] = 0ull;
     }
   };
@@ -694,9 +802,9 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
 template <int WAVES, int G, int DEPTH>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(const uint32_t* gptr, const unsigned short* x, int K,
                                                                 int Kc, int KC, float tau, int tile_slots, int seg_off,
-                                                                int scr_off, int misc_off, float max_abs, int R, int M,
-                                                                KernelArgs p) {
-  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, K, Kc, KC, tau, tile_slots, seg_off, scr_off, misc_off, max_abs, R, M}, p,
+                                                                int scr_off, int misc_off, const unsigned short* colmax,
+                                                                int R, int M, KernelArgs p) {
+  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, K, Kc, KC, tau, tile_slots, seg_off, scr_off, misc_off, colmax, R, M}, p,
                                 static_cast<int>(blockIdx.x));
 }
 
@@ -706,7 +814,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs b
   if (static_cast<int>(blockIdx.x) >= ba.blocks[pi]) return;   // past this product's grid
   const KernelArgs& p = ba.prod[pi];
   spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.K, p.Kc, p.KC, p.tau, p.tile_slots, p.seg_off, p.scr_off,
-                                      p.misc_off, p.max_abs, p.R, p.M},
+                                      p.misc_off, p.colmax, p.R, p.M},
                                 p, static_cast<int>(blockIdx.x));
 }
 
@@ -739,6 +847,7 @@ struct Plan {
 celty_status check_header(const celty_rlc_csc* W) {
   if (!W) return CELTY_EINVAL;
   if (W->version != CELTY_FORMAT_VERSION || W->run_bits != CELTY_RUN_BITS) return CELTY_EINVAL;
+  if (W->layout != CELTY_LAYOUT_RLC) return CELTY_EINVAL;
   if (W->M < 1 || W->K < 1 || W->R < 1) return CELTY_EINVAL;
   if (W->T != static_cast<int32_t>((static_cast<int64_t>(W->M) + W->R - 1) / W->R)) return CELTY_EINVAL;
   if (W->n_groups < 0 || W->n_groups > static_cast<int64_t>(UINT32_MAX)) return CELTY_EINVAL;
@@ -748,6 +857,7 @@ celty_status check_header(const celty_rlc_csc* W) {
   if (W->n_groups > 0 && (!W->values || !W->runs)) return CELTY_EINVAL;
   if (!(W->max_abs >= 0.f) || std::isinf(W->max_abs)) return CELTY_EINVAL;
   if (misaligned(W->values, 16) || misaligned(W->runs, 4)) return CELTY_EINVAL;
+  if (!W->colmax || misaligned(W->colmax, 4)) return CELTY_EINVAL;
   return CELTY_OK;
 }
 
@@ -803,7 +913,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   pl.scr_off = static_cast<int>(off);
   off += static_cast<size_t>(pl.waves) * kWave * pl.groups * 4;
   pl.misc_off = static_cast<int>(off);
-  off += static_cast<size_t>(3 * pl.waves) * 4;   // the block scan's per-wavefront totals
+  off += static_cast<size_t>(4 * pl.waves) * 4;   // the block scan's per-wavefront totals, then the sums of U
   pl.lds = align_up(off, 16);
   if (pl.lds > static_cast<size_t>(kMaxLds)) return CELTY_EINVAL;
   pl.blocks = static_cast<int64_t>(W->T) * pl.KC;
@@ -843,7 +953,7 @@ celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stre
     const KernelArgs& q = a.prod[0];
     hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.max_blocks)),
                        dim3(WAVES * kWave), ln.lds, stream, q.gptr, q.x, q.K, q.Kc, q.KC, q.tau, q.tile_slots,
-                       q.seg_off, q.scr_off, q.misc_off, q.max_abs, q.R, q.M, q);
+                       q.seg_off, q.scr_off, q.misc_off, q.colmax, q.R, q.M, q);
   } else {
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_batch_kernel<WAVES, G, DEPTH>, batch_attr))
       return CELTY_EHIP;
@@ -890,19 +1000,8 @@ celty_status product_args(const celty_rlc_csc* W, const Plan& pl, const void* x,
   a.x = static_cast<const unsigned short*>(x);
   a.y = static_cast<unsigned short*>(y);
   a.ws = static_cast<unsigned long long*>(ws);
-  // merge scale: any row sum is at most K * max|w| * 65504 (the largest
-  // finite fp16 |x|); 2^s_glob maps that bound to at most 2^48
-  a.s_glob = 0;
-  {
-    const double bound = static_cast<double>(W->K) * static_cast<double>(W->max_abs) * 65504.0;
-    if (bound > 0.0) {
-      int e;
-      std::frexp(bound, &e);
-      a.s_glob = 48 - e;
-    }
-  }
+  a.colmax = W->colmax;
   a.tau = tau;
-  a.max_abs = W->max_abs;
   a.n_groups = static_cast<uint32_t>(W->n_groups);
   a.M = W->M;
   a.K = W->K;

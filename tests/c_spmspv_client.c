@@ -54,7 +54,7 @@ int main(int argc, char** argv) {
   if (!W || !mask || !x) return 2;
 
   int64_t G = 0, nnz = 0, pad = 0;
-  celty_status st = celty_encode_plan(W, K, mask, K, M, K, R, &G, &nnz, &pad);
+  celty_status st = celty_encode_plan(W, K, mask, K, M, K, R, CELTY_LAYOUT_RLC, &G, &nnz, &pad);
   if (st != CELTY_OK) return 3;
   const int32_t T = (M + R - 1) / R;
   const size_t n_gptr = (size_t)T * (size_t)K + 1;
@@ -62,28 +62,32 @@ int main(int argc, char** argv) {
   uint16_t* values = NULL;
   if (posix_memalign((void**)&values, 16, (size_t)(8 * G + 8) * 2) != 0) return 3;
   uint32_t* runs = (uint32_t*)malloc((size_t)(G + 1) * 4);
+  uint16_t* colmax = (uint16_t*)malloc((size_t)K * 2 + 4);
   celty_rlc_csc enc;
-  if (!gptr || !runs) return 3;
-  st = celty_encode(W, K, mask, K, M, K, R, gptr, values, runs, G, &enc, 0);
+  if (!gptr || !runs || !colmax) return 3;
+  st = celty_encode(W, K, mask, K, M, K, R, CELTY_LAYOUT_RLC, gptr, values, runs, colmax, G, &enc, 0);
   if (st != CELTY_OK) return 3;
 
-  void *d_gptr, *d_values, *d_runs, *d_x, *d_y, *d_ws;
+  void *d_gptr, *d_values, *d_runs, *d_colmax, *d_x, *d_y, *d_ws;
   const size_t ws_bytes = celty_spmspv_workspace_bytes(M, K, R);
   HIP_OK(hipMalloc(&d_gptr, n_gptr * 4));
   HIP_OK(hipMalloc(&d_values, (size_t)(8 * G + 8) * 2));
   HIP_OK(hipMalloc(&d_runs, (size_t)(G + 1) * 4));
+  HIP_OK(hipMalloc(&d_colmax, (size_t)K * 2));
   HIP_OK(hipMalloc(&d_x, (size_t)K * 2));
   HIP_OK(hipMalloc(&d_y, (size_t)M * 2));
   HIP_OK(hipMalloc(&d_ws, ws_bytes));
   HIP_OK(hipMemcpy(d_gptr, gptr, n_gptr * 4, hipMemcpyHostToDevice));
   HIP_OK(hipMemcpy(d_values, values, (size_t)(8 * G) * 2, hipMemcpyHostToDevice));
   HIP_OK(hipMemcpy(d_runs, runs, (size_t)G * 4, hipMemcpyHostToDevice));
+  HIP_OK(hipMemcpy(d_colmax, colmax, (size_t)K * 2, hipMemcpyHostToDevice));
   HIP_OK(hipMemcpy(d_x, x, (size_t)K * 2, hipMemcpyHostToDevice));
 
   celty_rlc_csc dev = enc;   /* same header, device arrays */
   dev.gptr = (const uint32_t*)d_gptr;
   dev.values = (const uint16_t*)d_values;
   dev.runs = (const uint32_t*)d_runs;
+  dev.colmax = (const uint16_t*)d_colmax;
   st = celty_spmspv_workspace_init(d_ws, ws_bytes, NULL);
   if (st == CELTY_OK) st = celty_spmspv(&dev, d_x, tau, d_y, d_ws, ws_bytes, NULL);
   if (st != CELTY_OK) {
@@ -100,9 +104,10 @@ int main(int argc, char** argv) {
   HIP_OK(hipFree(d_gptr));
   HIP_OK(hipFree(d_values));
   HIP_OK(hipFree(d_runs));
+  HIP_OK(hipFree(d_colmax));
   HIP_OK(hipFree(d_x));
   HIP_OK(hipFree(d_y));
   HIP_OK(hipFree(d_ws));
-  free(W); free(mask); free(x); free(gptr); free(values); free(runs); free(y);
+  free(W); free(mask); free(x); free(gptr); free(values); free(runs); free(colmax); free(y);
   return 0;
 }

@@ -57,13 +57,14 @@ void round_trip(int M, int K, int R, double keep, double long_gap_rows, bool wit
   }
   const uint8_t* mp = with_mask ? mask.data() : nullptr;
   int64_t G = 0, nnz = 0, pad = 0;
-  check(celty_encode_plan(W.data(), ldw, mp, ldm, M, K, R, &G, &nnz, &pad) == CELTY_OK, "plan", M, K, R);
+  check(celty_encode_plan(W.data(), ldw, mp, ldm, M, K, R, CELTY_LAYOUT_RLC, &G, &nnz, &pad) == CELTY_OK, "plan", M, K, R);
   const int T = (M + R - 1) / R;
   std::vector<uint32_t> gptr(static_cast<size_t>(T) * K + 1);
   // values must be 16-byte aligned: over-allocate and align
   std::vector<uint16_t> vbuf(static_cast<size_t>(8 * G + 8));
   uint16_t* values = reinterpret_cast<uint16_t*>((reinterpret_cast<uintptr_t>(vbuf.data()) + 15u) & ~uintptr_t{15});
   std::vector<uint32_t> runs(static_cast<size_t>(G) + 1);
+  std::vector<uint16_t> colmax(static_cast<size_t>(K));
   std::vector<uint16_t> Wd(static_cast<size_t>(M) * K);
   std::vector<uint8_t> md(static_cast<size_t>(M) * K);
   const int thread_counts[3] = {1, 3, 0};
@@ -72,7 +73,8 @@ void round_trip(int M, int K, int R, double keep, double long_gap_rows, bool wit
   for (int ti = 0; ti < 3; ++ti) {
     celty_rlc_csc enc;
     std::memset(&enc, 0, sizeof(enc));
-    check(celty_encode(W.data(), ldw, mp, ldm, M, K, R, gptr.data(), values, runs.data(), G, &enc,
+    check(celty_encode(W.data(), ldw, mp, ldm, M, K, R, CELTY_LAYOUT_RLC, gptr.data(), values, runs.data(),
+                       colmax.data(), G, &enc,
                        thread_counts[ti]) == CELTY_OK,
           "encode", M, K, R);
     check(enc.n_groups == G && enc.n_nnz == nnz && enc.n_pad == pad, "header counts", M, K, R);
@@ -101,7 +103,8 @@ void round_trip(int M, int K, int R, double keep, double long_gap_rows, bool wit
   if (T * K >= 2 && G > 0) {
     celty_rlc_csc enc;
     std::memset(&enc, 0, sizeof(enc));
-    celty_encode(W.data(), ldw, mp, ldm, M, K, R, gptr.data(), values, runs.data(), G, &enc, 1);
+    celty_encode(W.data(), ldw, mp, ldm, M, K, R, CELTY_LAYOUT_RLC, gptr.data(), values, runs.data(), colmax.data(), G,
+                 &enc, 1);
     std::vector<uint32_t> bad(gptr);
     bad[1] = static_cast<uint32_t>(G) + 1u;
     enc.gptr = bad.data();
@@ -112,20 +115,21 @@ void round_trip(int M, int K, int R, double keep, double long_gap_rows, bool wit
 void error_paths() {
   uint16_t w[4] = {0x3C00u, 0, 0x3C00u, 0};
   int64_t G = 0, nnz = 0, pad = 0;
-  check(celty_encode_plan(nullptr, 2, nullptr, 2, 2, 2, 1, &G, &nnz, &pad) == CELTY_EINVAL, "null W", 2, 2, 1);
-  check(celty_encode_plan(w, 1, nullptr, 2, 2, 2, 1, &G, &nnz, &pad) == CELTY_EINVAL, "short stride", 2, 2, 1);
-  check(celty_encode_plan(w, 2, nullptr, 2, 2, 2, 0, &G, &nnz, &pad) == CELTY_EINVAL, "R = 0", 2, 2, 0);
-  check(celty_encode_plan(w, 2, nullptr, 2, 2, 2, 1, nullptr, &nnz, &pad) == CELTY_EINVAL, "null output", 2, 2, 1);
-  check(celty_encode_plan(w, 2, nullptr, 2, 2, 2, 1, &G, &nnz, &pad) == CELTY_OK, "plan ok", 2, 2, 1);
+  check(celty_encode_plan(nullptr, 2, nullptr, 2, 2, 2, 1, CELTY_LAYOUT_RLC, &G, &nnz, &pad) == CELTY_EINVAL, "null W", 2, 2, 1);
+  check(celty_encode_plan(w, 1, nullptr, 2, 2, 2, 1, CELTY_LAYOUT_RLC, &G, &nnz, &pad) == CELTY_EINVAL, "short stride", 2, 2, 1);
+  check(celty_encode_plan(w, 2, nullptr, 2, 2, 2, 0, CELTY_LAYOUT_RLC, &G, &nnz, &pad) == CELTY_EINVAL, "R = 0", 2, 2, 0);
+  check(celty_encode_plan(w, 2, nullptr, 2, 2, 2, 1, CELTY_LAYOUT_RLC, nullptr, &nnz, &pad) == CELTY_EINVAL, "null output", 2, 2, 1);
+  check(celty_encode_plan(w, 2, nullptr, 2, 2, 2, 1, CELTY_LAYOUT_RLC, &G, &nnz, &pad) == CELTY_OK, "plan ok", 2, 2, 1);
   uint32_t gptr[8];
   alignas(16) uint16_t values[64];
   uint32_t runs[8];
+  alignas(4) uint16_t cmax[2];
   celty_rlc_csc enc;
-  check(celty_encode(w, 2, nullptr, 2, 2, 2, 1, gptr, values + 1, runs, G, &enc, 1) == CELTY_EINVAL,
+  check(celty_encode(w, 2, nullptr, 2, 2, 2, 1, CELTY_LAYOUT_RLC, gptr, values + 1, runs, cmax, G, &enc, 1) == CELTY_EINVAL,
         "misaligned values", 2, 2, 1);
-  check(celty_encode(w, 2, nullptr, 2, 2, 2, 1, gptr, values, runs, G + 1, &enc, 1) == CELTY_EINVAL,
+  check(celty_encode(w, 2, nullptr, 2, 2, 2, 1, CELTY_LAYOUT_RLC, gptr, values, runs, cmax, G + 1, &enc, 1) == CELTY_EINVAL,
         "group count mismatch", 2, 2, 1);
-  check(celty_encode(w, 2, nullptr, 2, 2, 2, 1, gptr, values, runs, G, &enc, -1) == CELTY_EINVAL,
+  check(celty_encode(w, 2, nullptr, 2, 2, 2, 1, CELTY_LAYOUT_RLC, gptr, values, runs, cmax, G, &enc, -1) == CELTY_EINVAL,
         "negative thread count", 2, 2, 1);
   check(celty_decode(nullptr, nullptr, nullptr) == CELTY_EINVAL, "decode null", 0, 0, 0);
 }

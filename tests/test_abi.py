@@ -78,16 +78,20 @@ def test_encode_plan_rejects_bad_arguments():
     W = np.ones((4, 5), dtype=np.float16).view(np.uint16)
     g, n, p = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     f = celty._encode_plan
-    ok = f(W.ctypes.data, 5, None, 0, 4, 5, 2, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p))
+    ok = f(W.ctypes.data, 5, None, 0, 4, 5, 2, 0, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p))
     assert ok == CELTY_OK and n.value == 20 and p.value == 0 and g.value == 10
-    assert f(None, 5, None, 0, 4, 5, 2, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
-    assert f(W.ctypes.data, 4, None, 0, 4, 5, 2, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
-    assert f(W.ctypes.data, 5, W.ctypes.data, 3, 4, 5, 2, ctypes.byref(g), ctypes.byref(n),
+    assert f(None, 5, None, 0, 4, 5, 2, 0, ctypes.byref(g), ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
+    assert f(W.ctypes.data, 4, None, 0, 4, 5, 2, 0, ctypes.byref(g), ctypes.byref(n),
+             ctypes.byref(p)) == CELTY_EINVAL
+    assert f(W.ctypes.data, 5, W.ctypes.data, 3, 4, 5, 2, 0, ctypes.byref(g), ctypes.byref(n),
              ctypes.byref(p)) == CELTY_EINVAL
     for M, K, R in ((0, 5, 2), (4, 0, 2), (4, 5, 0)):
-        assert f(W.ctypes.data, 5, None, 0, M, K, R, ctypes.byref(g), ctypes.byref(n),
+        assert f(W.ctypes.data, 5, None, 0, M, K, R, 0, ctypes.byref(g), ctypes.byref(n),
                  ctypes.byref(p)) == CELTY_EINVAL
-    assert f(W.ctypes.data, 5, None, 0, 4, 5, 2, None, ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
+    assert f(W.ctypes.data, 5, None, 0, 4, 5, 2, 0, None, ctypes.byref(n), ctypes.byref(p)) == CELTY_EINVAL
+    for layout in (-1, 3, 99):                                       # unknown layouts
+        assert f(W.ctypes.data, 5, None, 0, 4, 5, 2, layout, ctypes.byref(g), ctypes.byref(n),
+                 ctypes.byref(p)) == CELTY_EINVAL
 
 
 def test_encode_rejects_bad_arguments():
@@ -95,14 +99,25 @@ def test_encode_rejects_bad_arguments():
     gptr = celty._aligned_empty(3 * 5 + 1, np.uint32)
     vals = celty._aligned_empty(8 * 20, np.uint16)
     runs = celty._aligned_empty(20, np.uint32)
+    cmax = celty._aligned_empty(6, np.uint16)
     d = celty_rlc_csc()
     f = celty._encode
-    args = [W.ctypes.data, 5, None, 0, 4, 5, 2, gptr.ctypes.data, vals.ctypes.data, runs.ctypes.data]
+    args = [W.ctypes.data, 5, None, 0, 4, 5, 2, 0, gptr.ctypes.data, vals.ctypes.data, runs.ctypes.data,
+            cmax.ctypes.data]
     assert f(*args, 10, ctypes.byref(d), 1) == CELTY_OK
+    assert cmax[:5].view(np.float16).tolist() == [1.0] * 5 and d.colmax == cmax.ctypes.data
     assert f(*args, 11, ctypes.byref(d), 1) == CELTY_EINVAL          # n_groups mismatch
     assert f(*args, 10, ctypes.byref(d), -1) == CELTY_EINVAL         # n_threads
     bad = list(args)
-    bad[8] = vals.ctypes.data + 2                                    # values not 16-byte aligned
+    bad[9] = vals.ctypes.data + 2                                    # values not 16-byte aligned
+    assert f(*bad, 10, ctypes.byref(d), 1) == CELTY_EINVAL
+    bad = list(args)
+    bad[11] = cmax.ctypes.data + 2                                   # colmax not 4-byte aligned
+    assert f(*bad, 10, ctypes.byref(d), 1) == CELTY_EINVAL
+    bad[11] = None                                                   # no colmax
+    assert f(*bad, 10, ctypes.byref(d), 1) == CELTY_EINVAL
+    bad = list(args)
+    bad[7] = 5                                                       # unknown layout
     assert f(*bad, 10, ctypes.byref(d), 1) == CELTY_EINVAL
     assert f(*args, 10, None, 1) == CELTY_EINVAL
 
@@ -127,8 +142,16 @@ def test_decode_rejects_corrupt_streams():
     d4.T += 1                                                        # inconsistent header
     assert celty._decode(ctypes.byref(d4), out.ctypes.data, m.ctypes.data) == CELTY_EINVAL
     d5 = enc.desc()
-    d5.version = 2
+    d5.version = 1
     assert celty._decode(ctypes.byref(d5), out.ctypes.data, m.ctypes.data) == CELTY_EINVAL
+    cm = enc.colmax.copy()
+    cm[2] = np.uint16(int(cm[2]) + 1)                               # column maximum disagrees
+    d6 = enc.desc()
+    d6.colmax = cm.ctypes.data
+    assert celty._decode(ctypes.byref(d6), out.ctypes.data, m.ctypes.data) == CELTY_EFORMAT
+    d7 = enc.desc()
+    d7.colmax = None
+    assert celty._decode(ctypes.byref(d7), out.ctypes.data, m.ctypes.data) == CELTY_EINVAL
 
 
 # --------------------------------------------------------------------------
@@ -149,7 +172,8 @@ FAKE = 0x7F0000000000   # never dereferenced: every call below fails validation 
 
 def _desc(M=4096, K=4096, R=256, G=1000):
     T = -(-M // R)
-    return celty_rlc_csc(1, M, K, R, T, 4, G, 8 * G, 7 * G, G, 1.0, 0, FAKE, FAKE + 0x10000, FAKE + 0x20000)
+    return celty_rlc_csc(celty.FORMAT_VERSION, M, K, R, T, 4, G, 8 * G, 7 * G, G, 1.0, 0, FAKE, FAKE + 0x10000,
+                         FAKE + 0x20000, FAKE + 0x30000)
 
 
 @host_only
@@ -220,7 +244,8 @@ def test_spmspv_plan_is_host_only():
 @host_only
 @pytest.mark.parametrize("case", ["null_desc", "version", "run_bits", "T", "values_align", "runs_align",
                                   "null_x", "nan_tau", "x_align", "overlap", "short_ws", "null_ws",
-                                  "ws_align", "waves", "max_abs_nan", "max_abs_inf", "max_abs_neg", "slices"])
+                                  "ws_align", "waves", "max_abs_nan", "max_abs_inf", "max_abs_neg", "slices",
+                                  "null_colmax", "colmax_align", "layout"])
 def test_spmspv_rejects_bad_arguments(case):
     d = _desc()
     x, y, ws = FAKE + 0x100000, FAKE + 0x200000, FAKE + 0x300000
@@ -228,7 +253,7 @@ def test_spmspv_rejects_bad_arguments(case):
     nws = celty.celty_spmspv_workspace_bytes(4096, 4096, 256)
     launch = None
     if case == "version":
-        d.version = 2
+        d.version = 1
     elif case == "run_bits":
         d.run_bits = 3
     elif case == "T":
@@ -261,6 +286,12 @@ def test_spmspv_rejects_bad_arguments(case):
         d.max_abs = math.inf
     elif case == "max_abs_neg":
         d.max_abs = -1.0
+    elif case == "null_colmax":
+        d.colmax = None
+    elif case == "colmax_align":
+        d.colmax += 2
+    elif case == "layout":
+        d.layout = 7
     pd = None if case == "null_desc" else ctypes.byref(d)
     st = celty._spmspv_ex(pd, x, tau, y, ws, nws, None if launch is None else ctypes.byref(launch), None)
     assert st == CELTY_EINVAL
@@ -309,7 +340,7 @@ def test_batch_rejects_bad_arguments(case):
     elif case == "null_y":
         yp = None
     elif case == "bad_header":
-        descs[2].version = 2
+        descs[2].version = 1
     elif case == "nan_tau":
         tp[2] = math.nan
     elif case == "y_over_other_x":
@@ -381,8 +412,10 @@ class _FakeDeviceTensor:
 
     is_cuda = True
 
-    def __init__(self, numel, element_size, device="cuda:0"):
+    def __init__(self, numel, element_size, device="cuda:0", dtype=None):
+        import torch
         self._n, self._e, self.device = numel, element_size, device
+        self.dtype = dtype if dtype is not None else {1: torch.uint8, 2: torch.int16, 4: torch.int32}[element_size]
 
     def is_contiguous(self):
         return True
@@ -407,14 +440,18 @@ class _FakeEncoded:
 
 
 @host_only
-@pytest.mark.parametrize("case", ["x_short", "y_short", "x_device", "y_device", "ws_device"])
+@pytest.mark.parametrize("case", ["x_short", "y_short", "x_device", "y_device", "ws_device", "x_bf16", "y_bf16"])
 def test_binding_rejects_short_or_misplaced_tensors(case):
     """The C ABI takes bare pointers and trusts x to hold K halves and y M, so
-    the binding checks the tensors' sizes and device before calling it."""
+    the binding checks the tensors' sizes, dtype and device before calling it
+    (a bfloat16 tensor has 2-byte elements too, but is not fp16)."""
+    import torch
     M, K = 300, 200
     W = _FakeEncoded(M, K)
-    x = _FakeDeviceTensor(K - 1 if case == "x_short" else K, 2, "cuda:1" if case == "x_device" else "cuda:0")
-    y = _FakeDeviceTensor(M - 1 if case == "y_short" else M, 2, "cuda:1" if case == "y_device" else "cuda:0")
+    x = _FakeDeviceTensor(K - 1 if case == "x_short" else K, 2, "cuda:1" if case == "x_device" else "cuda:0",
+                          torch.bfloat16 if case == "x_bf16" else None)
+    y = _FakeDeviceTensor(M - 1 if case == "y_short" else M, 2, "cuda:1" if case == "y_device" else "cuda:0",
+                          torch.bfloat16 if case == "y_bf16" else None)
     ws = _FakeDeviceTensor(1 << 20, 1, "cuda:1" if case == "ws_device" else "cuda:0")
     with pytest.raises(ValueError):
         celty.celty_spmspv(W, x, 0.5, y, ws, stream=0)
@@ -436,3 +473,16 @@ def test_select_binding_rejects_short_or_misplaced_outputs(case):
     count = _FakeDeviceTensor(0 if case == "count_empty" else 1, 4)
     with pytest.raises(ValueError):
         celty.celty_select(x, 0.5, idx, count, stream=0)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64, np.int16, np.int32])
+def test_encoder_binding_accepts_only_fp16_weights(dtype):
+    """A float32 W viewed as uint16 would encode an M x 2K matrix of bit
+    halves; the binding refuses every dtype but float16 and uint16 bits."""
+    W = np.ones((4, 6), dtype=dtype)
+    with pytest.raises(ValueError):
+        celty.celty_encode(W, None, 2)
+    with pytest.raises(ValueError):
+        celty.celty_encode_plan(W, None, 2)
+    ok = celty.celty_encode(np.ones((4, 6), np.float16).view(np.uint16), None, 2)
+    assert ok.n_nnz == 24

@@ -1,6 +1,6 @@
 """The library's host encoder is bit-exact with the oracle's encoder.
 
-gptr, values, runs and the header counts must match exactly, for any tile
+gptr, values, runs, colmax and the header counts must match exactly, for any tile
 height R, thread count, odd shapes, kept +-0 weights, empty and full columns,
 and at the full 4096 x 4096 / 11008 x 4096 sizes of the benchmark configs.
 """
@@ -20,6 +20,8 @@ def _assert_same(enc, ref):
     assert np.array_equal(enc.gptr, ref.gptr)
     assert np.array_equal(enc.values, ref.values)
     assert np.array_equal(enc.runs, ref.runs)
+    assert np.array_equal(enc.colmax, ref.colmax)
+    assert enc.max_abs == float(ref.colmax.view(np.float16).astype(np.float32).max(initial=0.0))
 
 
 SHAPES = [(1, 1, 1), (1, 9, 4), (9, 1, 4), (7, 8, 3), (64, 64, 64), (65, 63, 16), (200, 31, 1000),

@@ -716,3 +716,93 @@ def test_large_weights_and_activations(celty, torch_dev):
     _note("large magnitudes")
     y = _run(celty, torch_dev, W, mask, x, tau, 512)
     _check(y, W, mask, x, tau)
+
+
+# --------------------------------------------------------------------------
+# the fused selection where each lane scans several columns (Section 3.1's
+# column skip, m = ceil(columns / lanes) of 2 to 8)
+# --------------------------------------------------------------------------
+def _identity_x(seed, K, nan_every=0, grid=None):
+    rng = np.random.default_rng(seed)
+    x = rng.laplace(size=K)
+    if grid:
+        x = np.round(x * grid) / grid          # every value a multiple of 1/grid
+    x = x.astype(np.float16)
+    if nan_every:
+        x[::nan_every] = np.float16(np.nan)
+    return x
+
+
+@pytest.mark.parametrize("launch", [(1000, 2, 1), (4096, 8, 1), (4096, 16, 1), (300, 2, 1), (2048, 4, 1),
+                                    (1000, 2, 2), (4096, 8, 4)])
+@pytest.mark.parametrize("case", ["tau", "nan", "tau_negative"])
+def test_identity_pattern_several_columns_per_lane(celty, torch_dev, launch, case):
+    K = 4096
+    I = np.eye(K, dtype=np.float16)
+    lanes = 64 * launch[1]
+    m = -(-min(launch[0], K) // lanes)
+    tau = 0.8
+    if case == "tau":
+        x = _identity_x(11, K)
+    elif case == "nan":
+        x = _identity_x(12, K, nan_every=7)
+    else:
+        # every non-NaN column active, zeros included; the values sit on a
+        # grid of 2^-6 so that each single-term row lands exactly on the
+        # fixed-point grid
+        x = _identity_x(13, K, nan_every=11, grid=64)
+        tau = -1.0
+    _note(f"identity K={K} launch={launch} ({m} columns per lane) {case}")
+    assert 2 <= m <= 8
+    y = _run(celty, torch_dev, I, None, x, tau, 512, launch=launch)
+    xf = x.astype(np.float32)
+    want = np.where(np.abs(xf) > tau, x, np.float16(0)).astype(np.float16)   # NaN fails the test
+    assert np.array_equal(y.view(np.uint16), want.view(np.uint16))
+
+
+# --------------------------------------------------------------------------
+# the benchmark configurations at the remaining seeds and layers
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("seed", [1, 2, 3, 4])
+@pytest.mark.parametrize("ws", [30, 50, 70])
+@pytest.mark.parametrize("as_", [30, 50, 70])
+def test_config2_sweep_other_seeds(celty, torch_dev, seed, ws, as_):
+    p = workloads.make_problem(2, 4096, 4096, ws, as_, "laplace", seed=seed, proj=7)
+    _full(celty, torch_dev, p, f"config2 seed{seed} ws{ws} as{as_}")
+
+
+@pytest.mark.parametrize("layer", [1, 7, 13, 20, 26, 33, 38])
+def test_config4_more_layers(celty, torch_dev, layer):
+    for p in workloads.layer_problems(4, 0, layer):
+        _full(celty, torch_dev, p, f"config4 layer{layer} {p.meta['proj_name']}")
+
+
+@pytest.mark.parametrize("as_", [40, 60, 80])
+def test_config5_last_layer(celty, torch_dev, as_):
+    # layer 79 of the 80-layer step: every projection at as60, the distinct
+    # shapes at as40 and as80
+    names = ("q", "k", "v", "o", "gate", "up", "down") if as_ == 60 else ("q", "k", "gate", "down")
+    for p in workloads.layer_problems(5, 0, 79, as_):
+        if p.meta["proj_name"] in names:
+            _full(celty, torch_dev, p, f"config5 layer79 as{as_} {p.meta['proj_name']}")
+
+
+@pytest.mark.parametrize("M,K,R", [(3000, 2500, 256), (4096, 4097, 512), (1500, 33, 64)])
+def test_x_only_two_byte_aligned(celty, torch_dev, M, K, R):
+    # x at an odd 2-byte offset: the merge bound is summed one column per load
+    # instead of two (the same terms, another order)
+    torch, dev = torch_dev
+    p = workloads.random_small(M + K, M, K, ws=50, as_=50)
+    Wd = celty.celty_encode(p.W, p.mask, R).to_device(dev)
+    buf = torch.zeros(K + 1, dtype=torch.int16, device=dev)
+    buf[1:] = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    x = buf[1:]
+    assert x.data_ptr() % 4 == 2
+    y = torch.empty(M, dtype=torch.int16, device=dev)
+    ws = celty.new_workspace(Wd, dev)
+    _note(f"x 2-byte aligned M={M} K={K} R={R}")
+    for launch in (None, (64, 2, 1)):
+        celty.celty_spmspv_ex(Wd, x, p.tau, y, ws, launch)
+        torch.cuda.synchronize()
+        assert int(ws.count_nonzero()) == 0
+        _check(y.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
