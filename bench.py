@@ -782,8 +782,9 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f16 inputs, f32 products, i32/i64 fixed-point sums",
         "arithmetic": "fp16 W and x; every product exact in fp32; sums in int32 fixed point per workgroup on a "
-                      "grid from the sum of colmax*|x| over its active columns, merged across column slices "
-                      "in int64 on a grid from the same sum over every active column; y fp16 (RNE)",
+                      "grid from n * max colmax*|x| over its n active columns; column slices merged with 64-bit "
+                      "integer atomics on a fixed 2^-33 grid (partials clamped to +-4096, the excess added on "
+                      "2^-8); y fp16 (RNE)",
         "data": "synthetic",
         "config": {"workload": workload, "workload_key": workload_key, "M": M, "K": K, "weight_sparsity_pct": args.ws,
                    "activation_sparsity_pct": args.as_, "tile_rows_R": R, "storage": "fp16 values + 4-bit runs",

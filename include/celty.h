@@ -175,8 +175,8 @@ typedef struct celty_launch {
  * 0 when M < 1. */
 int32_t celty_default_tile_rows(int32_t M, int32_t K);
 
-/* Bytes of device workspace celty_spmspv needs for this shape: one 64-bit
- * merge slot per output row, rounded up to 256 bytes. */
+/* Bytes of device workspace celty_spmspv needs for this shape: two 64-bit
+ * merge words per output row, rounded up to 256 bytes. */
 size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R);
 
 /*
@@ -200,32 +200,32 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  *              bytes, zero-filled before first use (celty_spmspv_workspace_init).
  * One kernel launch.  The grid is (row tile t) x (column slice c).  Every
  * workgroup selects the active columns of its slice that store entries in
- * its tile (A_ct), walks their compressed segments, forms each product
- * w * x_k exactly in fp32 and adds it into an LDS tile of R int32 rows:
+ * its tile (the n columns of A_ct), walks their compressed segments, forms
+ * each product w * x_k exactly in fp32 and adds it into an LDS tile of R
+ * int32 rows:
  *
- *   B_ct = sum over k in A_ct of colmax[k] * |x_k|      (fp32)
+ *   B_ct = n * max over k in A_ct of colmax[k] * |x_k|   (fp32)
  *   s_ct = 30 - e(B_ct), where 2^(e-1) <= B_ct < 2^e     (clamped to [-64, 64])
  *
  * and each product is rounded to the nearest multiple of 2^-s_ct (ties
- * upward) before the integer add, so no partial sum can leave int32.  The
- * slices of a row tile are merged with one returning 64-bit atomic per row
- * and slice, in int64 fixed point on the launch-wide grid 2^-s_U:
+ * upward) before the integer add, so no partial sum can leave int32.  With
+ * one column slice, y[r] = fp16(fp32(tile[r]) * 2^-s_ct).  With several,
+ * the slices of a row tile are merged with one returning 64-bit atomic per
+ * row and slice: each partial p, clamped to +-4096, is added as a multiple
+ * of 2^-33 (ties upward); a clamped slice also adds p minus the clamp, as a
+ * multiple of 2^-8, to a second word of the row (an extra atomic, ordered
+ * before its ticket by a release fence).  The slice that arrives last
+ * writes y[r] = fp16(fp32(fine) * 2^-33 + fp32(excess) * 2^-8) and clears
+ * both words.  Error of a row r before those output roundings, for n_rc
+ * products of row r in slice c:
  *
- *   U   = sum over every active k of colmax[k] * |x_k|  (fp32, the same
- *         summation order in every workgroup, so all agree on it)
- *   s_U = 48 - e(U)                                      (clamped to [-64, 64])
+ *   |sum - exact| <= sum over slices c of n_rc * B_ct * 2^-30
+ *                    + 2^-34 per slice (2^-9 per slice whose partial was clamped)
  *
- * each slice's partial being rounded onto that grid (ties upward); the slice
- * that arrives last at a row writes y[row] = fp16(fp32(sum) * 2^-s_U) and
- * clears the slot.  With one slice the tile goes straight to y.  Error of a
- * row r before the final fp32 and fp16 roundings, for n_r products in the
- * row, KC slices and s_ct not clamped:
- *
- *   |sum - exact| <= sum over slices of n_rc * B_ct * 2^-30  +  KC * U * 2^-48
- *                 <= (n_r * 2^-30 + KC * 2^-48) * U,
- *
- * where U >= sum over k of |W[r,k] x_k| for every row r.  (fp32 accumulation
- * in any order has the worst case (n_r - 1) * 2^-24 * sum_k |W[r,k] x_k|.)
+ * (when s_ct is not clamped; B_ct bounds every row's sum of |products| in
+ * slice c).  The 2^-34 term, below half the spacing of fp16 subnormals, is
+ * the only one that does not scale with the data.  (An fp32 sum of n terms
+ * in any order has the worst case (n - 1) * 2^-24 * sum_k |W[r,k] x_k|.)
  * colmax must bound every |stored value| of its column (the encoder sets it
  * exactly): a smaller value can overflow the int32 tile and give wrong rows,
  * but never an access outside the arrays.

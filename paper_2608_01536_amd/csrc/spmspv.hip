@@ -21,17 +21,18 @@
 //     added into an LDS tile of the R output rows (Section 3.3's
 //     scatter-accumulation in on-chip memory).  The tile holds int32 fixed
 //     point on a per-workgroup grid 2^-s derived from the slice's own data:
-//     B = sum over its kept columns of colmax[k] * |x_k| bounds every row's
-//     sum of |products|, and 2^s puts B just below 2^30, so no row can
+//     B = n * max over its n kept columns of colmax[k] * |x_k| bounds every
+//     row's sum of |products|, and 2^s puts B just below 2^30, so no row can
 //     overflow (on gfx950 an LDS integer atomic add costs a small fraction of
 //     an fp32 one);
 //   * the slices of a row tile are merged with one returning 64-bit atomic
-//     per row: fixed point on a launch-wide grid plus an arrival count.  The
-//     grid comes from U = sum over every active column of colmax[k] * |x_k|,
-//     which every workgroup sums from x and colmax in the same order (so all
-//     agree on it) while its first compressed loads are in flight.  The slice
-//     that arrives last writes y[row] in fp16 and clears the slot for the
-//     next call.  With a single slice the tile goes straight to y.
+//     per row and slice on a fixed grid of 2^-33 (each slice's partial
+//     clamped to +-4096, far above the partials of LLM layers) plus an
+//     arrival count; a slice whose partial exceeds the clamp first adds the
+//     excess to a second word on a grid of 2^-8 and flags it in the first,
+//     so that the last slice also reads that word.  The slice that arrives
+//     last writes y[row] in fp16 and clears the words for the next call.
+//     With a single slice the tile goes straight to y.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -49,11 +50,33 @@ namespace {
 
 constexpr int kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kSlack = 8 + 128;       // tile rows past R: alignment entries, and the cap's reach
-constexpr int kMaxSlices = 63;        // column slices per row tile (merge ticket count byte)
+constexpr int kMaxSlices = 63;        // column slices per row tile (6-bit arrival count of the merge)
 constexpr int kMaxCols = 8;           // columns per thread in the selection
+// The merge's 64-bit ticket: a slice's clamped partial on the grid 2^-33
+// plus a bias of kFineClamp (= 4096 on that grid) in bits 0..51, the count
+// of clamped slices in bits 52..57 and the arrival count in bits 58..63.
+constexpr long long kFineClamp = 1ll << 45;
+constexpr unsigned long long kTicketExcess = 1ull << 52;
+constexpr unsigned long long kTicketCount = 1ull << 58;
 // Cache policy of the value loads: non-temporal (the nt bit of gfx950's
 // buffer loads), so the streamed weights do not displace cached lines.
 constexpr int kStreamPolicy = 2;
+
+// Dynamic LDS of a workgroup (byte offsets; the int32 tile is at 0): the
+// tile of R rows plus 7 alignment rows and 128 rows of slack that bound where
+// a corrupt stream could write (a group base is capped at R + 7 and a group
+// adds at most 128); the selection's list of Kc segments; the walk's scratch
+// (64 * G ints per wavefront); the block scan's per-wavefront totals (3 words
+// each).  The host sizes the launch with the same function.
+struct LdsLayout {
+  int tile_slots, seg_off, scr_off, misc_off, bytes;
+};
+__host__ __device__ constexpr int align16(int v) { return (v + 15) & ~15; }
+__host__ __device__ constexpr LdsLayout lds_layout(int R, int Kc, int waves, int groups) {
+  return LdsLayout{R + kSlack, align16(4 * (R + kSlack)), align16(4 * (R + kSlack)) + 16 * Kc,
+                   align16(4 * (R + kSlack)) + 16 * Kc + 256 * waves * groups,
+                   align16(align16(4 * (R + kSlack)) + 16 * Kc + 256 * waves * groups + 12 * waves)};
+}
 
 struct SegInfo {
   uint32_t gstart;   // first group of the segment in the values/runs arrays
@@ -74,6 +97,17 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// The same pattern with max: lane 63 ends with the wavefront maximum.
+__device__ __forceinline__ uint32_t wave_inclusive_max(uint32_t v) {
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x142, 0xA, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x143, 0xC, 0xF, false)));
+  return v;
+}
+
 // Inclusive scan over the 16 lanes of each DPP row.
 __device__ __forceinline__ uint32_t row_inclusive_scan(uint32_t v) {
   v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false));
@@ -82,52 +116,43 @@ __device__ __forceinline__ uint32_t row_inclusive_scan(uint32_t v) {
   v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false));
   return v;
 }
-
-// Sum over the 64 lanes (every lane gets it): DPP row shifts and broadcasts
-// in a fixed order, so the same inputs give the same bits in every wavefront.
-__device__ __forceinline__ float wave_sum(float v) {
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x111, 0xF, 0xF, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x112, 0xF, 0xF, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x114, 0xF, 0xF, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x118, 0xF, 0xF, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), kWave - 1));
+__device__ __forceinline__ uint32_t row_inclusive_max(uint32_t v) {
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, false)));
+  return v;
 }
 
-// Block-wide: exclusive scans of a and b, their totals, and the sum of the
-// non-negative floats f (WAVES <= 16).  Each wavefront's totals go to part[]
-// (3*WAVES words, used once per launch); after the barrier lane l < WAVES of
-// every wavefront reads wavefront l's totals and one row scan gives the
-// offsets of all wavefronts.
+// Block-wide: exclusive scans of a and b, their totals, and the maximum of m
+// (WAVES <= 16).  Each wavefront's totals go to part[] (3*WAVES words, used
+// once per launch); after the barrier lane l < WAVES of every wavefront reads
+// wavefront l's totals and one row scan gives the offsets of all wavefronts.
 template <int WAVES>
-__device__ __forceinline__ void block_scan_select(uint32_t a, uint32_t b, float f, uint32_t& ea, uint32_t& eb,
-                                                  uint32_t& ta, uint32_t& tb, float& tf, uint32_t* part) {
+__device__ __forceinline__ void block_scan_select(uint32_t a, uint32_t b, uint32_t m, uint32_t& ea, uint32_t& eb,
+                                                  uint32_t& ta, uint32_t& tb, uint32_t& tm, uint32_t* part) {
   static_assert(WAVES <= 16, "one DPP row holds the per-wavefront totals");
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
   const uint32_t ia = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(a)));
   const uint32_t ib = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(b)));
-  const float sf = wave_sum(f);
+  const uint32_t im = wave_inclusive_max(m);
   if (lane == kWave - 1) {
     part[wv] = ia;
     part[WAVES + wv] = ib;
-    part[2 * WAVES + wv] = __float_as_uint(sf);
+    part[2 * WAVES + wv] = im;
   }
   __syncthreads();
-  uint32_t pa = 0, pb = 0;
-  float pf = 0.f;
+  uint32_t pa = 0, pb = 0, pm = 0;
   if (lane < WAVES) {
     pa = part[lane];
     pb = part[WAVES + lane];
-    pf = __uint_as_float(part[2 * WAVES + lane]);
+    pm = part[2 * WAVES + lane];
   }
-  const uint32_t sa = row_inclusive_scan(pa), sb = row_inclusive_scan(pb);
+  const uint32_t sa = row_inclusive_scan(pa), sb = row_inclusive_scan(pb), sm = row_inclusive_max(pm);
   ta = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sa), WAVES - 1));
   tb = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sb), WAVES - 1));
-  tf = 0.f;
-#pragma unroll
-  for (int w = 0; w < WAVES; ++w) tf += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pf), w));
+  tm = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sm), WAVES - 1));
   const uint32_t oa = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sa - pa), wv));
   const uint32_t ob = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(sb - pb), wv));
   ea = oa + ia - a;
@@ -140,84 +165,6 @@ __device__ __forceinline__ void block_scan_select(uint32_t a, uint32_t b, float 
 __device__ __forceinline__ int grid_scale(float b, int top) {
   if (!(b > 0.f)) return 0;
   return min(max(top - __builtin_amdgcn_frexp_expf(b), -64), 64);
-}
-
-// |x| * m for the fp16 halves x and m of two words (the product of two fp16
-// values is exact in fp32), or 0 unless |x| > tau (a NaN x fails the test).
-__device__ __forceinline__ float bound_term(uint32_t xbits, uint32_t mbits, float tau) {
-  const float ax = fabsf(half_bits_to_float(xbits & 0xFFFFu));
-  return ax > tau ? ax * half_bits_to_float(mbits & 0xFFFFu) : 0.f;
-}
-
-// The launch-wide bound U = sum over the active columns k < K of
-// colmax[k] * |x_k|.  Every workgroup sums the same terms in the same order:
-// lane tid of the workgroup takes the column pairs (2d, 2d+1) for
-// d = tid + j * NT (two fp16 per 32-bit load, from x and from colmax), then
-// the wavefronts' sums are added in wavefront order.  The loads of up to
-// kBoundPairs pairs per lane are issued first (issue) and summed later
-// (partial), so that they can overlap other memory traffic; pairs beyond
-// that, an odd last column and an x that is only 2-byte aligned are loaded
-// and summed in partial itself.
-constexpr int kBoundPairs = 16;
-struct BoundLoads {
-  uint32_t xw[kBoundPairs], mw[kBoundPairs];
-};
-
-__device__ __forceinline__ bool bound_fast(const unsigned short* x) {
-  return (reinterpret_cast<uintptr_t>(x) & 3u) == 0;
-}
-
-template <int NT>
-__device__ __forceinline__ void bound_issue(BoundLoads& bl, const unsigned short* x, const unsigned short* colmax,
-                                            int K) {
-  const int pairs = K >> 1;
-  if (!bound_fast(x) || pairs == 0) return;   // workgroup-uniform
-  const auto xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned short*>(x), static_cast<short>(0), 4 * pairs,
-                                                    0x00020000);
-  const auto mr = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned short*>(colmax), static_cast<short>(0),
-                                                    4 * pairs, 0x00020000);
-  const int nj = min((pairs + NT - 1) / NT, kBoundPairs);
-#pragma unroll
-  for (int j = 0; j < kBoundPairs; ++j) {
-    bl.xw[j] = bl.mw[j] = 0u;
-    if (j < nj) {   // workgroup-uniform; pairs past the end read as zero
-      const int off = 4 * (static_cast<int>(threadIdx.x) + j * NT);
-      bl.xw[j] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0);
-      bl.mw[j] = __builtin_amdgcn_raw_buffer_load_b32(mr, off, 0, 0);
-    }
-  }
-}
-
-// This lane's part of U (see bound_issue), summed over the wavefront.
-template <int NT>
-__device__ __forceinline__ float bound_partial(const BoundLoads& bl, const unsigned short* x,
-                                               const unsigned short* colmax, int K, float tau) {
-  float acc = 0.f;
-  const int tid = static_cast<int>(threadIdx.x);
-  if (bound_fast(x)) {
-    const int pairs = K >> 1;
-    const int nj = (pairs + NT - 1) / NT;
-#pragma unroll
-    for (int j = 0; j < kBoundPairs; ++j) {
-      if (j < nj) {
-        acc += bound_term(bl.xw[j], bl.mw[j], tau);
-        acc += bound_term(bl.xw[j] >> 16, bl.mw[j] >> 16, tau);
-      }
-    }
-    for (int j = kBoundPairs; j < nj; ++j) {
-      const int d = tid + j * NT;
-      if (d < pairs) {
-        const uint32_t xw = reinterpret_cast<const uint32_t*>(x)[d];
-        const uint32_t mw = reinterpret_cast<const uint32_t*>(colmax)[d];
-        acc += bound_term(xw, mw, tau);
-        acc += bound_term(xw >> 16, mw >> 16, tau);
-      }
-    }
-    if ((K & 1) && tid == 0) acc += bound_term(x[K - 1], colmax[K - 1], tau);
-  } else {
-    for (int k = tid; k < K; k += NT) acc += bound_term(x[k], colmax[k], tau);
-  }
-  return wave_sum(acc);
 }
 
 // Start of wavefront w's range of the slice's n_grp groups.  A SIMD holds
@@ -493,12 +440,11 @@ struct KernelArgs {
   const uint32_t* runs;
   const unsigned short* x;      // fp16 bits
   unsigned short* y;            // fp16 bits
-  unsigned long long* ws;       // [M] merge tickets (see the merge below)
+  unsigned long long* ws;       // [2M] merge words (see the merge below)
   const unsigned short* colmax; // [K] fp16 bits: largest |stored weight| of each column
   float tau;
   uint32_t n_groups;
-  int M, K, R, Kc, KC, tile_slots;
-  int seg_off, scr_off, misc_off;   // byte offsets into dynamic LDS (the tile is at 0)
+  int M, K, R, Kc, KC;
 };
 
 // Up to kMaxBatch independent products in one launch: grid (max blocks, n),
@@ -512,7 +458,7 @@ struct BatchArgs {
 };
 
 // The arguments a workgroup's prologue needs (the selection's pointers and
-// sizes, the LDS layout, the column maxima, R and M).  A single-product launch passes
+// sizes, the column maxima, R and M; the LDS layout follows from R and Kc).  A single-product launch passes
 // them as leading kernel arguments, which gfx950 preloads into scalar
 // registers at dispatch (the library is built with
 // -amdgpu-kernarg-preload-count), so neither the selection's first memory
@@ -520,10 +466,9 @@ struct BatchArgs {
 struct Early {
   const uint32_t* gptr;
   const unsigned short* x;
+  const unsigned short* colmax;
   int K, Kc, KC;
   float tau;
-  int tile_slots, seg_off, scr_off, misc_off;   // LDS layout
-  const unsigned short* colmax;
   int R, M;
 };
 
@@ -536,10 +481,10 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // the tile's LDS byte address (for the accumulation's own LDS instructions)
   const uint32_t tile_lds = static_cast<uint32_t>(
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem));
-  SegInfo* seg = reinterpret_cast<SegInfo*>(smem + e.seg_off);
-  int* scr_all = reinterpret_cast<int*>(smem + e.scr_off);
-  uint32_t* part = reinterpret_cast<uint32_t*>(smem + e.misc_off);   // 3*WAVES: the selection's scan
-  float* part_u = reinterpret_cast<float*>(smem + e.misc_off) + 3 * WAVES;   // WAVES: sums of U
+  const LdsLayout lay = lds_layout(e.R, e.Kc, WAVES, G);
+  SegInfo* seg = reinterpret_cast<SegInfo*>(smem + lay.seg_off);
+  int* scr_all = reinterpret_cast<int*>(smem + lay.scr_off);
+  uint32_t* part = reinterpret_cast<uint32_t*>(smem + lay.misc_off);   // 3*WAVES: the selection's scan
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   const int t = blk / e.KC, c = blk - t * e.KC;
@@ -580,17 +525,18 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   const int rows = min(e.R, e.M - row0);
   const int base4_cap = 4 * (e.R + 7);   // tile byte address cap of a group base
 
-  for (int i = tid; i < e.tile_slots; i += NT) tile[i] = 0;
+  for (int i = tid; i < lay.tile_slots; i += NT) tile[i] = 0;
   for (int i = tid; i < NT * G; i += NT) scr_all[i] = 0;
   int scale = 0;   // the workgroup's fixed-point scale 2^scale
 
   // ---- selection of this slice's active, non-empty columns ----------------
   // The flat group sequence is then cut into equal ranges, one per
   // wavefront (a segment may be shared by several).
-  // B = sum over the kept columns of colmax[k] * |x_k| bounds the sum of
-  // |products| of every row of the slice; the tile's grid 2^-scale puts B
-  // just below 2^30 (float rounding of B and the products' half-unit
-  // roundings stay far inside int32)
+  // B = n * max over the n kept columns of colmax[k] * |x_k| bounds the sum
+  // of |products| of every row of the slice; the tile's grid 2^-scale puts B
+  // just below 2^30 (the products' half-unit roundings stay far inside
+  // int32).  Non-negative floats order like their bit patterns, so the
+  // maximum is an integer scan.
   uint32_t n_seg, n_grp;
   if (one_per_lane) {
     // one column per lane
@@ -598,18 +544,16 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     const float xv = half_bits_to_float(xr[0]);
     const bool keep = tid < kn && fabsf(xv) > e.tau && g1 > g0;
     const uint32_t cnt = keep ? g1 - g0 : 0u;
-    uint32_t en, eg;
-    float bound;
-    block_scan_select<WAVES>(keep ? 1u : 0u, cnt, keep ? fabsf(xv) * half_bits_to_float(cm[0]) : 0.f, en, eg,
-                             n_seg, n_grp, bound, part);
-    const int s = grid_scale(bound, 30);
+    uint32_t en, eg, tmax;
+    block_scan_select<WAVES>(keep ? 1u : 0u, cnt, keep ? __float_as_uint(fabsf(xv) * half_bits_to_float(cm[0])) : 0u,
+                             en, eg, n_seg, n_grp, tmax, part);
+    const int s = grid_scale(static_cast<float>(n_seg) * __uint_as_float(tmax), 30);
     if (keep) seg[en] = SegInfo{g0, eg, cnt, ldexpf(xv, s)};
     scale = s;
   } else {
     // m <= kMaxCols consecutive columns per lane (loaded above), so one block
     // scan still orders all of them: segment order is column order
-    uint32_t keep_bits = 0u, n_loc = 0u, g_loc = 0u;
-    float b_loc = 0.f;
+    uint32_t keep_bits = 0u, n_loc = 0u, g_loc = 0u, m_loc = 0u;
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) {
       const float xv = half_bits_to_float(xr[j]);
@@ -617,12 +561,11 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
       keep_bits |= (keep ? 1u : 0u) << j;
       n_loc += keep ? 1u : 0u;
       g_loc += keep ? g[j + 1] - g[j] : 0u;
-      b_loc += keep ? fabsf(xv) * half_bits_to_float(cm[j]) : 0.f;
+      m_loc = max(m_loc, keep ? __float_as_uint(fabsf(xv) * half_bits_to_float(cm[j])) : 0u);
     }
-    uint32_t en, eg;
-    float bound;
-    block_scan_select<WAVES>(n_loc, g_loc, b_loc, en, eg, n_seg, n_grp, bound, part);
-    const int s = grid_scale(bound, 30);
+    uint32_t en, eg, tmax;
+    block_scan_select<WAVES>(n_loc, g_loc, m_loc, en, eg, n_seg, n_grp, tmax, part);
+    const int s = grid_scale(static_cast<float>(n_seg) * __uint_as_float(tmax), 30);
     uint32_t idx = en, off = eg;
 #pragma unroll
     for (int j = 0; j < kMaxCols; ++j) {
@@ -650,30 +593,19 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   const int wvu = __builtin_amdgcn_readfirstlane(wv);
   const uint32_t pb0 = cut_of<WAVES>(wvu, n_grp);
   const uint32_t pe = cut_of<WAVES>(wvu + 1, n_grp);
-  // The merge's bound U (several slices only): its loads go out before the
-  // ring's, and it is summed while the ring's first passes are in flight.
-  const bool merged = e.KC > 1;   // workgroup-uniform
-  BoundLoads bl;
-  if (merged) bound_issue<NT>(bl, e.x, e.colmax, e.K);
-  const bool has_work = pb0 < pe;   // wavefront-uniform
-  SegInfo s0{0u, 0u, 0u, 0.f};
-  int i_begin = 0;
-  const int i_end = static_cast<int>(n_seg);
-  const Streams st = make_streams(p.values, p.runs, p.n_groups);
-  int* scr = scr_all + wv * kWave * G;
-  const int n_pass = has_work ? static_cast<int>((pe - pb0 + P - 1) / P) : 0;
-  uint32_t before = 0u;
-  uint32_t rb[4] = {0u, 0u, 0u, 0u};
-  Pass<G> ring[DEPTH];
-  uint32_t pf = pb0;    // flat start of the next pass to fetch
-  int icur = 0;         // segment holding group pf
-  if (has_work) {
-    i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
+  if (pb0 < pe) {
+    SegInfo s0;
+    const int i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
+    const int i_end = static_cast<int>(n_seg);
+    const Streams st = make_streams(p.values, p.runs, p.n_groups);
+    int* scr = scr_all + wv * kWave * G;
+    const int n_pass = static_cast<int>((pe - pb0 + P - 1) / P);
     // A range that starts inside a segment starts at the row reached by the
     // segment's earlier groups: their runs (up to 4 * 64 groups here, the
     // rest below) are loaded ahead of the ring, so that their round trip
     // overlaps the ring's.
-    before = pb0 - s0.off;
+    const uint32_t before = pb0 - s0.off;
+    uint32_t rb[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (before > static_cast<uint32_t>(q * kWave)) {   // wavefront-uniform
@@ -683,19 +615,15 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
         rb[q] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + j) << 2), 0, 0);
       }
     }
-    icur = i_begin;
+    Pass<G> ring[DEPTH];
+    uint32_t pf = pb0;    // flat start of the next pass to fetch
+    int icur = i_begin;   // segment holding group pf
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) {
       fetch_pass<G>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
       icur = next_pass_segment<G>(ring[d], pf, i_end);
       pf += P;
     }
-  }
-  if (merged) {
-    const float u = bound_partial<NT>(bl, e.x, e.colmax, e.K, e.tau);
-    if (lane == 0) part_u[wv] = u;
-  }
-  if (has_work) {
     uint32_t pb = pb0;    // flat start of the pass being accumulated
     int carry = 0;        // 4 * sum of (run + 1) over its first segment's earlier groups
     if (before > 0u) {
@@ -726,85 +654,121 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   __syncthreads();
 
   // ---- merge --------------------------------------------------------------
-  if (!merged) {
+  if (e.KC == 1) {
     for (int r = tid; r < rows; r += NT)
       p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -scale));
     return;
   }
-  // Every slice adds one ticket per row with a returning 64-bit atomic: its
-  // partial sum as fixed point on the launch-wide grid 2^-s_glob plus a bias
-  // of 2^49 that keeps each ticket positive, and 1 in the count byte (bits
-  // 56..63).  s_glob puts U, which bounds every slice's partial and their
-  // sum, just below 2^48.  The slice whose atomic returns count KC-1 is the
-  // last for that row: old + its ticket is the complete sum, so it writes y
-  // and clears the slot for the next call.  KC <= 63 keeps the biased sum
-  // below 2^56.
-  float u_total = 0.f;   // the wavefronts' sums in wavefront order: the same bits in every workgroup
-#pragma unroll
-  for (int w = 0; w < WAVES; ++w) u_total += part_u[w];
-  const int s_glob = grid_scale(u_total, 48);
-  constexpr long long kBias = 1ll << 49;
-  constexpr unsigned long long kCount = 1ull << 56;
-  const int shift = s_glob - scale;
-  const auto fixed_at_launch_scale = [&](long long q) -> long long {
-    // a valid colmax keeps B within a rounding of U, so shift <= 19; the
-    // clamp only keeps a wrong one from an undefined shift
-    if (shift >= 0) return q * (1ll << min(shift, 30));
-    const int rs = -shift;   // round half up onto the coarser grid
-    return rs > 62 ? 0 : ((q + (1ll << (rs - 1))) >> rs);
+  // Row r of the product owns two 64-bit words of the workspace: ws[r]
+  // collects tickets, ws[M + r] the excesses.  Every slice adds one ticket
+  // per row with a returning atomic: its partial p, clamped to +-4096, as a
+  // multiple of 2^-33 (at most 2^45 in magnitude) plus a bias of 2^45 that
+  // keeps it non-negative (bits 0..51), 1 in the arrival count (bits 58..63)
+  // and, when p was clamped, 1 in the excess count (bits 52..57).  KC <= 63
+  // slices keep each field from carrying into the next.  A slice whose p
+  // exceeds the clamp first adds p minus the clamp, as a multiple of 2^-8, to
+  // ws[M + r], and the wavefront's release fence orders that add before its
+  // tickets.  The slice whose atomic returns count KC-1 holds the complete
+  // sum of the clamped partials; when the excess count is non-zero it also
+  // reads ws[M + r] (after an acquire fence).  It writes y[r] and clears the
+  // words for the next call.
+  const auto ticket_of = [&](int q, bool& over, long long& excess) -> unsigned long long {
+    // p = q * 2^-scale; over iff |p| > 4096 = 2^12
+    const int s = scale;
+    const long long aq = q < 0 ? -static_cast<long long>(q) : static_cast<long long>(q);
+    over = s >= 19 ? false : (s >= -12 ? aq > (1ll << (s + 12)) : q != 0);
+    long long fine = 0;
+    excess = 0;
+    if (!over) {
+      const int sh = 33 - s;   // onto the grid 2^-33; |q| <= 4096 * 2^s keeps |fine| <= 2^45
+      if (q != 0) fine = sh >= 0 ? static_cast<long long>(q) * (1ll << min(sh, 45))
+                                 : ((static_cast<long long>(q) + (1ll << (-sh - 1))) >> -sh);
+    } else {
+      fine = q < 0 ? -kFineClamp : kFineClamp;
+      const int sh = 8 - s;   // the excess onto the grid 2^-8 (s < 19, so sh > -11)
+      const long long v = sh >= 0 ? static_cast<long long>(q) * (1ll << min(sh, 32))
+                                  : ((static_cast<long long>(q) + (1ll << (-sh - 1))) >> -sh);
+      // beyond +-2^48 (so far past fp16's range that the row is +-inf either
+      // way) the excess is clamped, so that 63 of them cannot overflow int64
+      const long long ex = v - (q < 0 ? -(1ll << 20) : (1ll << 20)), lim = 1ll << 56;
+      excess = ex < -lim ? -lim : (ex > lim ? lim : ex);
+    }
+    return kTicketCount + (over ? kTicketExcess : 0ull) + static_cast<unsigned long long>(fine + kFineClamp);
   };
   const auto finish_row = [&](int r, unsigned long long ticket, unsigned long long old) {
-    if ((old >> 56) == static_cast<unsigned long long>(e.KC - 1)) {
-      const long long total = static_cast<long long>((old & (kCount - 1)) + (ticket & (kCount - 1))) -
-                              static_cast<long long>(e.KC) * kBias;
-      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(total), -s_glob));
+    const unsigned long long sum = old + ticket;
+    const bool last = (old >> 58) == static_cast<unsigned long long>(e.KC - 1);
+    const bool excess = last && ((sum >> 52) & 63ull) != 0ull;
+    if (last) {
+      const long long fine = static_cast<long long>(sum & (kTicketExcess - 1)) -
+                             static_cast<long long>(e.KC) * kFineClamp;
+      float v = ldexpf(static_cast<float>(fine), -33);
+      if (excess) {
+        const long long c = static_cast<long long>(
+            __hip_atomic_load(p.ws + e.M + row0 + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        v += ldexpf(static_cast<float>(c), -8);
+        p.ws[e.M + row0 + r] = 0ull;
+      }
+      p.y[row0 + r] = float_to_half_bits(v);
       p.ws[row0 + r] = 0ull;
     }
   };
-  if (rows <= NT) {   // workgroup-uniform: one row per lane
-    if (tid < rows) {
-      const unsigned long long ticket = kCount + static_cast<unsigned long long>(fixed_at_launch_scale(tile[tid]) + kBias);
-      finish_row(tid, ticket, atomicAdd(p.ws + row0 + tid, ticket));
-    }
-    return;
-  }
-  // Taller tiles: a lane's rows go J at a time (J = 2 up to twice the
-  // workgroup's lanes, else 4), their atomics issued back to back under the
-  // execution mask (rows past a partial last tile issue none), then their
-  // returns are examined.
+  // a lane's rows go J at a time (J = 1 when the tile has no more rows than
+  // the workgroup has lanes, 2 up to twice that, else 4), their atomics
+  // issued back to back under the execution mask (rows past a partial last
+  // tile issue none: a shared dummy slot would serialise every such lane of
+  // every slice on one address), then their returns are examined
   const auto merge_rows = [&](auto in_flight) {
     constexpr int J = decltype(in_flight)::value;
-    for (int r0 = tid; r0 < rows; r0 += J * NT) {
+    for (int r0 = tid; r0 - tid < rows; r0 += J * NT) {
       unsigned long long ticket[J], old[J];
+      bool over[J];
+      long long excess[J];
+      bool any_over = false;
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         const int r = r0 + j * NT;
         ticket[j] = 0ull;
-        old[j] = 0ull;
-        // rows past the tile take no atomic: a shared dummy slot would
-        // serialise every such lane of every slice on one address
-        if (r < rows) {
-          ticket[j] = kCount + static_cast<unsigned long long>(fixed_at_launch_scale(tile[r]) + kBias);
-          old[j] = atomicAdd(p.ws + row0 + r, ticket[j]);
-        }
+        over[j] = false;
+        excess[j] = 0;
+        if (r < rows) ticket[j] = ticket_of(tile[r], over[j], excess[j]);
+        any_over |= over[j];
       }
+      if (__ballot(any_over) != 0ull) {   // wavefront-uniform; rare: partials beyond the clamp
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+          if (over[j]) atomicAdd(p.ws + e.M + row0 + r0 + j * NT, static_cast<unsigned long long>(excess[j]));
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      }
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        old[j] = 0ull;
+        if (r0 + j * NT < rows) old[j] = atomicAdd(p.ws + row0 + r0 + j * NT, ticket[j]);
+      }
+      bool excess_seen = false;
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        excess_seen |= r0 + j * NT < rows && (old[j] >> 58) == static_cast<unsigned long long>(e.KC - 1) &&
+                       (((old[j] + ticket[j]) >> 52) & 63ull) != 0ull;
+      if (__ballot(excess_seen) != 0ull) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // wavefront-uniform
 #pragma unroll
       for (int j = 0; j < J; ++j)
         if (r0 + j * NT < rows) finish_row(r0 + j * NT, ticket[j], old[j]);
     }
   };
-  if (rows <= 2 * NT)
+  if (rows <= NT)
+    merge_rows(std::integral_constant<int, 1>{});
+  else if (rows <= 2 * NT)
     merge_rows(std::integral_constant<int, 2>{});
   else
     merge_rows(std::integral_constant<int, 4>{});
 }
 
 template <int WAVES, int G, int DEPTH>
-__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(const uint32_t* gptr, const unsigned short* x, int K,
-                                                                int Kc, int KC, float tau, int tile_slots, int seg_off,
-                                                                int scr_off, int misc_off, const unsigned short* colmax,
-                                                                int R, int M, KernelArgs p) {
-  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, K, Kc, KC, tau, tile_slots, seg_off, scr_off, misc_off, colmax, R, M}, p,
+__global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(const uint32_t* gptr, const unsigned short* x,
+                                                                const unsigned short* colmax, int K, int Kc, int KC,
+                                                                float tau, int R, int M, KernelArgs p) {
+  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, colmax, K, Kc, KC, tau, R, M}, p,
                                 static_cast<int>(blockIdx.x));
 }
 
@@ -813,8 +777,7 @@ __global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs b
   const int pi = static_cast<int>(blockIdx.y);
   if (static_cast<int>(blockIdx.x) >= ba.blocks[pi]) return;   // past this product's grid
   const KernelArgs& p = ba.prod[pi];
-  spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.K, p.Kc, p.KC, p.tau, p.tile_slots, p.seg_off, p.scr_off,
-                                      p.misc_off, p.colmax, p.R, p.M},
+  spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.colmax, p.K, p.Kc, p.KC, p.tau, p.R, p.M},
                                 p, static_cast<int>(blockIdx.x));
 }
 
@@ -838,8 +801,7 @@ __global__ __launch_bounds__(256) void zero_fill_kernel(unsigned char* p, size_t
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Plan {
-  int waves = 4, groups = 1, Kc = 0, KC = 0, T = 0, tile_slots = 0;
-  int seg_off = 0, scr_off = 0, misc_off = 0;
+  int waves = 4, groups = 1, Kc = 0, KC = 0, T = 0;
   int64_t blocks = 0;
   size_t lds = 0;
 };
@@ -903,18 +865,8 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   // bank conflicts than the bookkeeping it saves
   pl.groups = (cfg && cfg->groups_per_lane) ? cfg->groups_per_lane : 1;
   if (pl.groups != 1 && pl.groups != 2 && pl.groups != 4) return CELTY_EINVAL;
-  // the tile (int32) goes first: R rows, then 7 alignment rows and 128 rows
-  // of slack that bound where a corrupt stream could write (base is capped at
-  // R + 7 and a group adds at most 128)
-  pl.tile_slots = W->R + kSlack;
-  size_t off = align_up(static_cast<size_t>(pl.tile_slots) * 4, 16);
-  pl.seg_off = static_cast<int>(off);
-  off += static_cast<size_t>(Kc) * sizeof(SegInfo);
-  pl.scr_off = static_cast<int>(off);
-  off += static_cast<size_t>(pl.waves) * kWave * pl.groups * 4;
-  pl.misc_off = static_cast<int>(off);
-  off += static_cast<size_t>(4 * pl.waves) * 4;   // the block scan's per-wavefront totals, then the sums of U
-  pl.lds = align_up(off, 16);
+  if (W->R > kMaxLds / 4) return CELTY_EINVAL;   // keeps the layout arithmetic in int
+  pl.lds = static_cast<size_t>(lds_layout(W->R, pl.Kc, pl.waves, pl.groups).bytes);
   if (pl.lds > static_cast<size_t>(kMaxLds)) return CELTY_EINVAL;
   pl.blocks = static_cast<int64_t>(W->T) * pl.KC;
   if (pl.blocks > 0x7FFFFFFF) return CELTY_EINVAL;
@@ -952,8 +904,8 @@ celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stre
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_kernel<WAVES, G, DEPTH>, single_attr)) return CELTY_EHIP;
     const KernelArgs& q = a.prod[0];
     hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.max_blocks)),
-                       dim3(WAVES * kWave), ln.lds, stream, q.gptr, q.x, q.K, q.Kc, q.KC, q.tau, q.tile_slots,
-                       q.seg_off, q.scr_off, q.misc_off, q.colmax, q.R, q.M, q);
+                       dim3(WAVES * kWave), ln.lds, stream, q.gptr, q.x, q.colmax, q.K, q.Kc, q.KC, q.tau, q.R,
+                       q.M, q);
   } else {
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_batch_kernel<WAVES, G, DEPTH>, batch_attr))
       return CELTY_EHIP;
@@ -1008,10 +960,6 @@ celty_status product_args(const celty_rlc_csc* W, const Plan& pl, const void* x,
   a.R = W->R;
   a.Kc = pl.Kc;
   a.KC = pl.KC;
-  a.tile_slots = pl.tile_slots;
-  a.seg_off = pl.seg_off;
-  a.scr_off = pl.scr_off;
-  a.misc_off = pl.misc_off;
   return CELTY_OK;
 }
 
@@ -1032,7 +980,7 @@ extern "C" size_t celty_spmspv_workspace_bytes(int32_t M, int32_t K, int32_t R) 
   (void)K;
   (void)R;
   if (M < 1) return 0;
-  return align_up(static_cast<size_t>(M) * 8, 256);
+  return align_up(static_cast<size_t>(M) * 16, 256);
 }
 
 extern "C" celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {

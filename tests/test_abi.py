@@ -65,9 +65,9 @@ def test_default_tile_rows():
 
 
 def test_workspace_bytes():
-    # one 64-bit merge slot per output row, rounded to 256 bytes
-    assert celty.celty_spmspv_workspace_bytes(4096, 4096, 256) == 4096 * 8
-    assert celty.celty_spmspv_workspace_bytes(1000, 7, 300) == 8192
+    # two 64-bit merge words per output row, rounded to 256 bytes
+    assert celty.celty_spmspv_workspace_bytes(4096, 4096, 256) == 4096 * 16
+    assert celty.celty_spmspv_workspace_bytes(1000, 7, 300) == 16128
     assert celty.celty_spmspv_workspace_bytes(0, 1, 1) == 0
 
 
@@ -307,7 +307,7 @@ def test_batch_workspace_bytes():
     descs = [_desc(M=4096), _desc(M=1000, K=300, R=128), _desc(M=11008, R=1024)]
     arr = (ctypes.POINTER(celty_rlc_csc) * 3)(*[ctypes.pointer(d) for d in descs])
     want = sum(celty.celty_spmspv_workspace_bytes(d.M, d.K, d.R) for d in descs)
-    assert celty._batch_ws_bytes(3, arr) == want == 4096 * 8 + 8192 + 11008 * 8
+    assert celty._batch_ws_bytes(3, arr) == want == 4096 * 16 + 16128 + 11008 * 16
     assert celty._batch_ws_bytes(0, arr) == 0
     assert celty._batch_ws_bytes(9, arr) == 0
     assert celty._batch_ws_bytes(2, None) == 0

@@ -10,7 +10,9 @@ magnitudes where a grid derived from anything else would be too coarse:
   smallest active |x|; and with tau < 0, a tiny x_k), so that it meets a
   small factor;
 * activations scaled by 1e-3 and 1e-4 (y shrinks with them), with and
-  without the outlier weight.
+  without the outlier weight;
+* slice partials beyond the merge's clamp of 4096 (the excess word), with
+  rows beyond fp16's range, which must come out infinite.
 
 Each case runs at the benchmark's 4096 x 4096 ws70/as70 problem and at the
 28672 x 8192 gate projection of the 70B-shaped configuration, in the
@@ -140,3 +142,33 @@ def test_scaled_activations(celty, torch_dev, shape, c, outlier):
     _note(f"{shape}: x * {c:g} (tau={tau:.4g}){' + inactive outlier' if outlier else ''}")
     y = _run(celty, torch_dev, W, mask, x, tau)
     _check(f"{shape} x*{c:g}{' outlier' if outlier else ''}", y, W, mask, x, tau)
+
+
+@pytest.mark.parametrize("launch", [None, (32, 2, 1), (64, 4, 1)])
+def test_partials_beyond_the_merge_clamp(celty, torch_dev, launch):
+    # weights ~N(0, 4^2) and activations ~Laplace * 200: slice partials of
+    # thousands, some beyond the merge's clamp of 4096, whose excess goes
+    # through the second merge word; rows beyond fp16's range become inf
+    torch, dev = torch_dev
+    rng = np.random.default_rng(12)
+    M, K = 2000, 600
+    W = (rng.standard_normal((M, K)) * 4).astype(np.float16)
+    mask = (rng.random((M, K)) < 0.5).astype(np.uint8)
+    x = (rng.laplace(size=K) * 200).astype(np.float16)
+    tau = workloads.tau_for_sparsity(x, 40)
+    Wd = celty.celty_encode(W, mask, 256).to_device(dev)
+    xt = torch.from_numpy(x.view(np.int16)).to(dev)
+    y = torch.empty(M, dtype=torch.int16, device=dev)
+    ws = celty.new_workspace(Wd, dev)
+    want = ref.spmspv_dense_fp64(W, mask, x, tau)
+    finite = np.abs(want) < 65504
+    _note(f"excess path launch={launch}: {int((~finite).sum())} rows beyond fp16")
+    for _ in range(2):   # twice: the excess words must be left zero as well
+        celty.celty_spmspv_ex(Wd, xt, tau, y, ws, launch)
+        torch.cuda.synchronize()
+        assert int(ws.count_nonzero()) == 0
+        got = y.cpu().numpy().view(np.float16)
+        assert np.all(np.isinf(got[~finite].astype(np.float32)) | (np.abs(want[~finite]) < 65520))
+        err = ref.rel_error(got[finite].astype(np.float64), want[finite])   # the finite rows on their own scale
+        _note(f"  rel_err={err:.3e}")
+        assert err <= TOL, err
