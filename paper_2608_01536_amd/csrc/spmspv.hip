@@ -667,43 +667,39 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // and, when p was clamped, 1 in the excess count (bits 52..57).  KC <= 63
   // slices keep each field from carrying into the next.  A slice whose p
   // exceeds the clamp first adds p minus the clamp, as a multiple of 2^-8, to
-  // ws[M + r], and the wavefront's release fence orders that add before its
+  // ws[M + r], and a release fence orders that add before the wavefront's
   // tickets.  The slice whose atomic returns count KC-1 holds the complete
   // sum of the clamped partials; when the excess count is non-zero it also
   // reads ws[M + r] (after an acquire fence).  It writes y[r] and clears the
   // words for the next call.
-  const auto ticket_of = [&](int q, bool& over, long long& excess) -> unsigned long long {
-    // p = q * 2^-scale; over iff |p| > 4096 = 2^12
-    const int s = scale;
-    const long long aq = q < 0 ? -static_cast<long long>(q) : static_cast<long long>(q);
-    over = s >= 19 ? false : (s >= -12 ? aq > (1ll << (s + 12)) : q != 0);
-    long long fine = 0;
-    excess = 0;
-    if (!over) {
-      const int sh = 33 - s;   // onto the grid 2^-33; |q| <= 4096 * 2^s keeps |fine| <= 2^45
-      if (q != 0) fine = sh >= 0 ? static_cast<long long>(q) * (1ll << min(sh, 45))
-                                 : ((static_cast<long long>(q) + (1ll << (-sh - 1))) >> -sh);
-    } else {
-      fine = q < 0 ? -kFineClamp : kFineClamp;
-      const int sh = 8 - s;   // the excess onto the grid 2^-8 (s < 19, so sh > -11)
-      const long long v = sh >= 0 ? static_cast<long long>(q) * (1ll << min(sh, 32))
-                                  : ((static_cast<long long>(q) + (1ll << (-sh - 1))) >> -sh);
-      // beyond +-2^48 (so far past fp16's range that the row is +-inf either
-      // way) the excess is clamped, so that 63 of them cannot overflow int64
-      const long long ex = v - (q < 0 ? -(1ll << 20) : (1ll << 20)), lim = 1ll << 56;
-      excess = ex < -lim ? -lim : (ex > lim ? lim : ex);
-    }
-    return kTicketCount + (over ? kTicketExcess : 0ull) + static_cast<unsigned long long>(fine + kFineClamp);
+  // Per workgroup: a partial q (units of 2^-scale) is clamped iff |q| > lim,
+  // i.e. |q * 2^-scale| > 4096; otherwise its ticket value is q * 2^(33 - scale)
+  // (rounded, ties upward, when the tile's grid is finer than 2^-33).
+  const int lim = scale >= 19 ? 0x7FFFFFFF : (scale >= -12 ? (1 << (scale + 12)) : 0);
+  const int sh = 33 - scale;
+  const auto fine_ticket = [&](int q) -> unsigned long long {
+    const long long f = sh >= 0 ? static_cast<long long>(q) * (1ll << min(sh, 45))
+                                : ((static_cast<long long>(q) + (1ll << (-sh - 1))) >> -sh);
+    return kTicketCount + static_cast<unsigned long long>(f + kFineClamp);
+  };
+  // the excess of a clamped partial on the grid 2^-8 (scale < 19 here)
+  const auto excess_of = [&](int q) -> long long {
+    const int se = 8 - scale;
+    const long long v = se >= 0 ? static_cast<long long>(q) * (1ll << min(se, 32))
+                                : ((static_cast<long long>(q) + (1ll << (-se - 1))) >> -se);
+    // beyond +-2^48 (so far past fp16's range that the row is +-inf either
+    // way) the excess is clamped, so that 63 of them cannot overflow int64
+    const long long ex = v - (q < 0 ? -(1ll << 20) : (1ll << 20)), cap = 1ll << 56;
+    return ex < -cap ? -cap : (ex > cap ? cap : ex);
   };
   const auto finish_row = [&](int r, unsigned long long ticket, unsigned long long old) {
     const unsigned long long sum = old + ticket;
-    const bool last = (old >> 58) == static_cast<unsigned long long>(e.KC - 1);
-    const bool excess = last && ((sum >> 52) & 63ull) != 0ull;
-    if (last) {
+    if ((old >> 58) == static_cast<unsigned long long>(e.KC - 1)) {
       const long long fine = static_cast<long long>(sum & (kTicketExcess - 1)) -
                              static_cast<long long>(e.KC) * kFineClamp;
       float v = ldexpf(static_cast<float>(fine), -33);
-      if (excess) {
+      if ((sum >> 52) & 63ull) {   // rare: some slice's partial was clamped
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         const long long c = static_cast<long long>(
             __hip_atomic_load(p.ws + e.M + row0 + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
         v += ldexpf(static_cast<float>(c), -8);
@@ -717,40 +713,30 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // the workgroup has lanes, 2 up to twice that, else 4), their atomics
   // issued back to back under the execution mask (rows past a partial last
   // tile issue none: a shared dummy slot would serialise every such lane of
-  // every slice on one address), then their returns are examined
+  // every slice on one address), then their returns are examined.  (The
+  // fences sit in the rare branches: a fence acts for the whole wavefront.)
   const auto merge_rows = [&](auto in_flight) {
     constexpr int J = decltype(in_flight)::value;
     for (int r0 = tid; r0 - tid < rows; r0 += J * NT) {
       unsigned long long ticket[J], old[J];
-      bool over[J];
-      long long excess[J];
-      bool any_over = false;
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         const int r = r0 + j * NT;
-        ticket[j] = 0ull;
-        over[j] = false;
-        excess[j] = 0;
-        if (r < rows) ticket[j] = ticket_of(tile[r], over[j], excess[j]);
-        any_over |= over[j];
-      }
-      if (__ballot(any_over) != 0ull) {   // wavefront-uniform; rare: partials beyond the clamp
-#pragma unroll
-        for (int j = 0; j < J; ++j)
-          if (over[j]) atomicAdd(p.ws + e.M + row0 + r0 + j * NT, static_cast<unsigned long long>(excess[j]));
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const int q = r < rows ? tile[r] : 0;
+        if ((q < 0 ? -q : q) <= lim) {
+          ticket[j] = fine_ticket(q);
+        } else {   // rare: the excess first, ordered before every ticket below
+          atomicAdd(p.ws + e.M + row0 + r, static_cast<unsigned long long>(excess_of(q)));
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+          ticket[j] = kTicketCount + kTicketExcess +
+                      static_cast<unsigned long long>((q < 0 ? -kFineClamp : kFineClamp) + kFineClamp);
+        }
       }
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         old[j] = 0ull;
         if (r0 + j * NT < rows) old[j] = atomicAdd(p.ws + row0 + r0 + j * NT, ticket[j]);
       }
-      bool excess_seen = false;
-#pragma unroll
-      for (int j = 0; j < J; ++j)
-        excess_seen |= r0 + j * NT < rows && (old[j] >> 58) == static_cast<unsigned long long>(e.KC - 1) &&
-                       (((old[j] + ticket[j]) >> 52) & 63ull) != 0ull;
-      if (__ballot(excess_seen) != 0ull) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // wavefront-uniform
 #pragma unroll
       for (int j = 0; j < J; ++j)
         if (r0 + j * NT < rows) finish_row(r0 + j * NT, ticket[j], old[j]);

@@ -144,8 +144,10 @@ def test_scaled_activations(celty, torch_dev, shape, c, outlier):
     _check(f"{shape} x*{c:g}{' outlier' if outlier else ''}", y, W, mask, x, tau)
 
 
-@pytest.mark.parametrize("launch", [None, (32, 2, 1), (64, 4, 1)])
-def test_partials_beyond_the_merge_clamp(celty, torch_dev, launch):
+@pytest.mark.parametrize("R,launch", [(256, None), (256, (32, 2, 1)), (256, (64, 4, 1)), (1024, (64, 2, 1)),
+                                      (1024, (96, 4, 1))])
+def test_partials_beyond_the_merge_clamp(celty, torch_dev, R, launch):
+    # (tiles of 1024 rows on 128 or 256 lanes: each lane merges 4 or 8 rows)
     # weights ~N(0, 4^2) and activations ~Laplace * 200: slice partials of
     # thousands, some beyond the merge's clamp of 4096, whose excess goes
     # through the second merge word; rows beyond fp16's range become inf
@@ -156,13 +158,13 @@ def test_partials_beyond_the_merge_clamp(celty, torch_dev, launch):
     mask = (rng.random((M, K)) < 0.5).astype(np.uint8)
     x = (rng.laplace(size=K) * 200).astype(np.float16)
     tau = workloads.tau_for_sparsity(x, 40)
-    Wd = celty.celty_encode(W, mask, 256).to_device(dev)
+    Wd = celty.celty_encode(W, mask, R).to_device(dev)
     xt = torch.from_numpy(x.view(np.int16)).to(dev)
     y = torch.empty(M, dtype=torch.int16, device=dev)
     ws = celty.new_workspace(Wd, dev)
     want = ref.spmspv_dense_fp64(W, mask, x, tau)
     finite = np.abs(want) < 65504
-    _note(f"excess path launch={launch}: {int((~finite).sum())} rows beyond fp16")
+    _note(f"excess path R={R} launch={launch}: {int((~finite).sum())} rows beyond fp16")
     for _ in range(2):   # twice: the excess words must be left zero as well
         celty.celty_spmspv_ex(Wd, xt, tau, y, ws, launch)
         torch.cuda.synchronize()
