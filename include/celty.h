@@ -267,6 +267,25 @@ celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const* W, const 
                                 const float* tau, void* const* y, void* workspace,
                                 size_t workspace_bytes, const celty_launch* launch, void* stream);
 
+/*
+ * As celty_spmspv_ex, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the merge words live in a static device array of the library
+ * (2 MiB on every GPU it runs on, held until the process ends) instead of a
+ * caller workspace, so the call takes no workspace and allocates nothing.
+ *   W, x, tau, y, launch, stream   as for celty_spmspv_ex.
+ * The array holds two 64-bit words per output row: M up to 131072.  Its
+ * device address is looked up once per device (hipGetSymbolAddress, with
+ * that device current); the first call on a device also zero-fills it with a
+ * kernel on `stream`, and every completed call leaves it zero.  Every call on
+ * a GPU shares that GPU's array: calls that overlap on one GPU (concurrent
+ * streams, or graphs replayed concurrently) race and give wrong rows.
+ * Errors: as celty_spmspv_ex, plus EINVAL when M exceeds 131072, EHIP when
+ *         the array's address cannot be found.
+ */
+celty_status celty_spmspv_noalloc(const celty_rlc_csc* W, const void* x, float tau, void* y,
+                                  const celty_launch* launch, void* stream);
+
 /* Workspace bytes of celty_spmspv_batch: the sum over the products of
  * celty_spmspv_workspace_bytes (host only; 0 for n outside 1..8 or null). */
 size_t celty_spmspv_batch_workspace_bytes(int32_t n, const celty_rlc_csc* const* W);

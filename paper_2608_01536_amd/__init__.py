@@ -78,6 +78,8 @@ _ws_init = _sig("celty_spmspv_workspace_init", ctypes.c_int, _p, _sz, _p)
 _spmspv = _sig("celty_spmspv", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz, _p)
 _spmspv_ex = _sig("celty_spmspv_ex", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz,
                   ctypes.POINTER(celty_launch), _p)
+_spmspv_noalloc = _sig("celty_spmspv_noalloc", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p,
+                       ctypes.POINTER(celty_launch), _p)
 _default_tile_rows = _sig("celty_default_tile_rows", _i32, _i32, _i32)
 _desc_pp = ctypes.POINTER(ctypes.POINTER(celty_rlc_csc))
 _batch = _sig("celty_spmspv_batch", ctypes.c_int, _i32, _desc_pp, ctypes.POINTER(_p), ctypes.POINTER(_f32),
@@ -311,6 +313,16 @@ def celty_spmspv_ex(W: DeviceRlcCsc, x, tau: float, y, workspace, launch=None, s
                       None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_ex")
 
 
+def celty_spmspv_noalloc(W: DeviceRlcCsc, x, tau: float, y, launch=None, stream=None) -> None:
+    """As celty_spmspv_ex with the library's static merge array (no workspace, nothing allocated)."""
+    d, dev = W.desc(), W.gptr.device
+    ls = _launch_struct(launch)
+    hd = _half_dtypes()
+    _check(_spmspv_noalloc(ctypes.byref(d), _dev_ptr(x, 2, "x", W.K, dev, hd), float(tau),
+                           _dev_ptr(y, 2, "y", W.M, dev, hd), None if ls is None else ctypes.byref(ls),
+                           _stream_handle(stream)), "celty_spmspv_noalloc")
+
+
 def _desc_array(Ws):
     descs = [W.desc() for W in Ws]
     arr = (ctypes.POINTER(celty_rlc_csc) * len(descs))(*[ctypes.pointer(d) for d in descs])
@@ -363,7 +375,7 @@ def default_tile_rows(M: int, K: int) -> int:
 __all__ = [
     "FORMAT_VERSION", "LAYOUT_RLC", "default_tile_rows",
     "celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv", "celty_spmspv_ex",
-    "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "new_batch_workspace",
+    "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "new_batch_workspace", "celty_spmspv_noalloc",
     "celty_spmspv_plan", "celty_spmspv_workspace_bytes", "celty_spmspv_workspace_init", "celty_status_string",
     "new_workspace", "HostRlcCsc", "DeviceRlcCsc", "CeltyError", "celty_rlc_csc", "celty_launch",
 ]

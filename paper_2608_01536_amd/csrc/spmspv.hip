@@ -39,9 +39,10 @@
 
 #include <algorithm>
 #include <atomic>
-#include <type_traits>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
+#include <type_traits>
 
 #include "celty.h"
 #include "common.h"
@@ -949,7 +950,49 @@ celty_status product_args(const celty_rlc_csc* W, const Plan& pl, const void* x,
   return CELTY_OK;
 }
 
+// The merge words of celty_spmspv_noalloc: a file-scope device array (one
+// copy on every GPU the library runs on, held until the process ends) in
+// place of a caller workspace.  Zero at load, zero-filled again by the first
+// call on each device, and left zero by every completed call.
+constexpr size_t kScratchBytes = size_t(2) << 20;   // two 64-bit words per row: M <= 131072
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device.  In host code the
+// array's name is only a stand-in for the symbol; its device address comes
+// from hipGetSymbolAddress, taken once per device (with that device current)
+// and kept.  The first call on a device also zero-fills the array on the
+// caller's stream (a kernel, so it may be recorded in a graph).
+std::mutex scratch_mutex;
+void* scratch_address[64] = {};
+
+celty_status scratch_on_current_device(hipStream_t stream, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return CELTY_EHIP;
+  if (dev < 0 || dev >= 64) return CELTY_EHIP;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_address[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return CELTY_EHIP;
+    hipLaunchKernelGGL(zero_fill_kernel, dim3(static_cast<unsigned>(kScratchBytes / 8 / 256)), dim3(256), 0, stream,
+                       static_cast<unsigned char*>(ptr), kScratchBytes);
+    if (hipGetLastError() != hipSuccess) return CELTY_EHIP;
+    scratch_address[dev] = ptr;
+  }
+  *out = scratch_address[dev];
+  return CELTY_OK;
+}
+
 }  // namespace
+
+extern "C" celty_status celty_spmspv_noalloc(const celty_rlc_csc* W, const void* x, float tau, void* y,
+                                             const celty_launch* launch_cfg, void* stream) {
+  if (celty_status st = check_header(W)) return st;
+  const size_t need = celty_spmspv_workspace_bytes(W->M, W->K, W->R);
+  if (need > kScratchBytes) return CELTY_EINVAL;   // more rows than the static array holds
+  void* ws = nullptr;
+  if (celty_status st = scratch_on_current_device(static_cast<hipStream_t>(stream), &ws)) return st;
+  return celty_spmspv_batch(1, &W, &x, &tau, &y, ws, need, launch_cfg, stream);
+}
 
 extern "C" int32_t celty_default_tile_rows(int32_t M, int32_t K) {
   if (M < 1) return 0;
