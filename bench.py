@@ -448,14 +448,10 @@ def fetched_bytes_from_encoding(enc, g_a: int, plan: dict) -> tuple:
     group pointers (each workgroup reads the Kc + 1 pointers of its slice in
     its row tile, so T * (K + KC) words).  total adds x and the column maxima
     of each workgroup's slice (2 + 2 B per column, once per row tile) and y
-    (2 B * M).  Returns (compressed, total, bound_pass): bound_pass is what
-    the workgroups read to sum the merge bound when there are several slices
-    (all of x and of the column maxima, 4 B * K each; L2 hits after the first
-    workgroup of an XCD)."""
+    (2 B * M).  Returns (compressed, total)."""
     KC = -(-enc.K // plan["cols_per_block"])
     compressed = 20 * g_a + 4 * enc.T * (enc.K + KC)
-    bound_pass = 4 * enc.K * enc.T * KC if KC > 1 else 0
-    return compressed, compressed + 4 * enc.T * enc.K + 2 * enc.M, bound_pass
+    return compressed, compressed + 4 * enc.T * enc.K + 2 * enc.M
 
 
 def stored_bytes(enc) -> int:
@@ -594,7 +590,7 @@ def paper_shapes(args) -> int:
             enc = celty.celty_encode(p.W, p.mask, R)
             plan = celty.celty_spmspv_plan(enc, None)
             b_alg, _, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
-            comp, _, _ = fetched_bytes_from_encoding(enc, g_a, plan)
+            comp, _ = fetched_bytes_from_encoding(enc, g_a, plan)
             sp_ = cold_spmspv(torch, celty, enc, p, None, args.steps, args.warmup, flush=flush)
             d = cold_dense(torch, F, p, args.steps, flush=flush)
             speed.setdefault(pct, []).append(d["us"] / sp_["us"])
@@ -740,7 +736,7 @@ def main() -> int:
         return record_kernel_trace(workload_key, args.record_kernel_trace, cmd)
     dev = torch.device("cuda:0")
     b_alg, e_a, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
-    comp_fetched, total_fetched, bound_pass = fetched_bytes_from_encoding(enc, g_a, plan)
+    comp_fetched, total_fetched = fetched_bytes_from_encoding(enc, g_a, plan)
     print(f"[bench] {M}x{K} ws{args.ws:g} as{args.as_:g} R={R} plan={plan}", file=sys.stderr, flush=True)
     flush = None if args.hot else CacheFlush(torch)
     run = cold_spmspv(torch, celty, enc, p, launch, args.steps, args.warmup, args.hot, flush=flush)
@@ -796,7 +792,6 @@ def main() -> int:
         "compressed_bytes_fetched": comp_fetched,
         "pct_peak_hbm_fetched": round(100 * comp_fetched / us_step / 1e3 / PEAK_HBM_GBPS, 2),
         "bytes_requested": total_fetched,
-        "bound_pass_bytes": bound_pass,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
                      "kernel_us": round(us_kernel, 3), "kernel_us_replays": [round(v, 3) for v in samples],
