@@ -18,9 +18,12 @@ spmspv   : activation selection by magnitude threshold and three independent
            evaluations of y = W (M o W) x_A: dense fp64, CSC fp64, brute force,
            plus a fp64 product that walks the RLC-CSC arrays the way the
            paper's kernel does.
+layouts  : two other encodings of the segments' rows: 16-bit absolute row
+           offsets (a decode-free form) and the lane-interleaved order of
+           Section 4.2, with their decoders.
 accounting: byte counts used for the roofline (algorithmic bytes per call)
            and the compression ratios the paper quotes (Section 3.2).
 
 Parity status of every function is listed in its docstring.
 """
-from . import rlc, spmspv, accounting  # noqa: F401
+from . import rlc, spmspv, accounting, layouts  # noqa: F401
