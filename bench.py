@@ -440,17 +440,18 @@ def algorithmic_bytes_from_encoding(enc, x: np.ndarray, tau: float) -> tuple:
     return 2.5 * e_a + 2.0 * enc.K + 2.0 * enc.M, e_a, g_a
 
 
-def fetched_bytes_from_encoding(enc, g_a: int, plan: dict) -> tuple:
+def fetched_bytes_from_encoding(enc, g_a: int, plan: dict, group_bytes: int = 20) -> tuple:
     """Bytes the kernel's own loads and stores request (merge atomics aside).
 
     compressed: every 8-entry group of an active column's segments (16 B of
-    values + 4 B of runs, the trailing alignment entries included) plus the
+    values + 4 B of runs, or 16 B of row offsets in the 16-bit row layout:
+    group_bytes; the trailing alignment entries included) plus the
     group pointers (each workgroup reads the Kc + 1 pointers of its slice in
     its row tile, so T * (K + KC) words).  total adds x and the column maxima
     of each workgroup's slice (2 + 2 B per column, once per row tile) and y
     (2 B * M).  Returns (compressed, total)."""
     KC = -(-enc.K // plan["cols_per_block"])
-    compressed = 20 * g_a + 4 * enc.T * (enc.K + KC)
+    compressed = group_bytes * g_a + 4 * enc.T * (enc.K + KC)
     return compressed, compressed + 4 * enc.T * enc.K + 2 * enc.M
 
 
@@ -663,6 +664,10 @@ def main() -> int:
                     help="outlier input features: per-feature scales exp(sigma*N(0,1)) on W's columns and x, "
                          "per-row magnitude pruning (0 = the uniform-mask workload)")
     ap.add_argument("--hot", action="store_true", help="reuse one copy (cache-resident; diagnostic)")
+    ap.add_argument("--layout", choices=("rlc", "rows16", "interleaved"), default="rlc",
+                    help="row encoding of the matrix: the paper's 4-bit runs (default), 16-bit row offsets "
+                         "(decode-free), or the runs in lane-interleaved order")
+    ap.add_argument("--lds-swizzle", action="store_true", help="XOR-swizzled LDS tile (RLC layout)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of a known size (counter calibration)")
     ap.add_argument("--record-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
@@ -707,21 +712,29 @@ def main() -> int:
     import workloads
 
     M, K = args.M, args.K
-    headline = (M, K, args.ws, args.as_) == (4096, 4096, 70.0, 70.0) and not args.sigma
+    headline = (M, K, args.ws, args.as_) == (4096, 4096, 70.0, 70.0) and not args.sigma and \
+        args.layout == "rlc" and not args.lds_swizzle
     if args.sigma:
         p = workloads.outlier_feature_problem(M, K, int(args.ws), args.as_, args.sigma)
     else:
         p = workloads.make_problem(2, M, K, args.ws, args.as_, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
     R = args.R or celty.default_tile_rows(M, K)
-    enc = celty.celty_encode(p.W, p.mask, R)
-    launch = (args.cols, args.waves) if (args.cols or args.waves) else None
+    layout = {"rlc": celty.LAYOUT_RLC, "rows16": celty.LAYOUT_ROWS16, "interleaved": celty.LAYOUT_INTERLEAVED}[args.layout]
+    enc_rlc = celty.celty_encode(p.W, p.mask, R)
+    enc = enc_rlc if layout == celty.LAYOUT_RLC else celty.celty_encode(p.W, p.mask, R, layout=layout)
+    swz = 1 if args.lds_swizzle else 0
+    launch = (args.cols, args.waves, 0, swz) if (args.cols or args.waves or swz) else None
     plan = celty.celty_spmspv_plan(enc, launch)
+    variant = ("" if layout == celty.LAYOUT_RLC else f"-{args.layout}") + ("-swizzle" if swz else "")
     workload_key = (f"{M}x{K}-ws{args.ws:g}-as{args.as_:g}" + (f"-sigma{args.sigma:g}" if args.sigma else "") + f"-R{R}-"
-                    f"{plan['cols_per_block']}x{plan['waves_per_block']}x{plan['groups_per_lane']}")
+                    f"{plan['cols_per_block']}x{plan['waves_per_block']}x{plan['groups_per_lane']}" + variant)
+    variant_flags = (f" --layout {args.layout}" if layout != celty.LAYOUT_RLC else "") + \
+                    (" --lds-swizzle" if swz else "")
     if args.record_traffic:
         flags = f" --M {M} --K {K} --ws {args.ws:g} --as {args.as_:g}" + (f" --R {args.R}" if args.R else "") + \
                 (f" --sigma {args.sigma:g}" if args.sigma else "") + \
-                (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "")
+                (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "") + \
+                variant_flags
         cmds = [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py "
                 f"--steps 200 --warmup 20 --no-cpu --no-dense{flags}" for c in ("FETCH_SIZE", "WRITE_SIZE")]
         cmds += [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py --copy-calibration"
@@ -730,13 +743,20 @@ def main() -> int:
     if args.record_kernel_trace:
         flags = f" --M {M} --K {K} --ws {args.ws:g} --as {args.as_:g}" + (f" --R {args.R}" if args.R else "") + \
                 (f" --sigma {args.sigma:g}" if args.sigma else "") + \
-                (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "")
+                (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "") + \
+                variant_flags
         cmd = (f"rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o run -- python3 bench.py "
                f"--no-cpu --no-dense --steps {args.steps} --warmup {args.warmup}{flags}")
         return record_kernel_trace(workload_key, args.record_kernel_trace, cmd)
     dev = torch.device("cuda:0")
-    b_alg, e_a, g_a = algorithmic_bytes_from_encoding(enc, p.x, p.tau)
-    comp_fetched, total_fetched = fetched_bytes_from_encoding(enc, g_a, plan)
+    # algorithmic bytes are those of the paper's format (RLC) for every
+    # variant; bytes requested are the variant's own
+    b_alg, e_a, g_a = algorithmic_bytes_from_encoding(enc_rlc, p.x, p.tau)
+    if layout == celty.LAYOUT_ROWS16:
+        g_v = algorithmic_bytes_from_encoding(enc, p.x, p.tau)[2]
+        comp_fetched, total_fetched = fetched_bytes_from_encoding(enc, g_v, plan, group_bytes=32)
+    else:
+        comp_fetched, total_fetched = fetched_bytes_from_encoding(enc, g_a, plan)
     print(f"[bench] {M}x{K} ws{args.ws:g} as{args.as_:g} R={R} plan={plan}", file=sys.stderr, flush=True)
     flush = None if args.hot else CacheFlush(torch)
     run = cold_spmspv(torch, celty, enc, p, launch, args.steps, args.warmup, args.hot, flush=flush)
@@ -783,7 +803,10 @@ def main() -> int:
                       "2^-8); y fp16 (RNE)",
         "data": "synthetic",
         "config": {"workload": workload, "workload_key": workload_key, "M": M, "K": K, "weight_sparsity_pct": args.ws,
-                   "activation_sparsity_pct": args.as_, "tile_rows_R": R, "storage": "fp16 values + 4-bit runs",
+                   "activation_sparsity_pct": args.as_, "tile_rows_R": R,
+                   "storage": {"rlc": "fp16 values + 4-bit runs", "rows16": "fp16 values + 16-bit row offsets",
+                               "interleaved": "fp16 values + 4-bit runs, lane-interleaved"}[args.layout] +
+                              (", XOR-swizzled LDS tile" if swz else ""),
                    "cold_copies": ncopies, "launch": plan},
         "effective_GBps": round(gbps_step, 1),
         "pct_peak_hbm": round(100 * gbps_step / PEAK_HBM_GBPS, 2),

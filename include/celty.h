@@ -51,7 +51,9 @@ typedef enum celty_status {
 #define CELTY_GROUP 8      /* entries per aligned group: one 16-byte fp16 vector */
 
 /* Layouts of the per-entry row information (the `layout` field). */
-#define CELTY_LAYOUT_RLC 0 /* 4-bit run lengths, Section 3.2 (the format below) */
+#define CELTY_LAYOUT_RLC 0         /* 4-bit run lengths, Section 3.2 (the format below) */
+#define CELTY_LAYOUT_ROWS16 1      /* 16-bit row offsets instead of runs (decode-free) */
+#define CELTY_LAYOUT_INTERLEAVED 2 /* the RLC entries in lane-interleaved order, Section 4.2 */
 
 /*
  * Tiled RLC-CSC, format version 2 (Section 3.2 plus the readings below).
@@ -77,6 +79,23 @@ typedef enum celty_status {
  * Version 1 was the same format without colmax.  The descriptor is plain
  * data; the arrays are owned by the caller and are host pointers for the
  * encoder/decoder and device pointers for celty_spmspv*.
+ *
+ * Two other layouts keep gptr, values, colmax and the 8-entry groups:
+ *  - CELTY_LAYOUT_ROWS16 (a decode-free form, for measuring what the run
+ *    reconstruction of Sections 3.3 and 4.2 costs): each entry carries its
+ *    row offset within the tile (0 .. R-1) as uint16; `runs` then points to
+ *    4 words per group, the uint16 at index 8g + j (little-endian) being
+ *    entry j's offset.  Only stored values are entries (no padding entries,
+ *    n_pad = 0); a segment's alignment entries have value 0 and repeat the
+ *    row offset of its last stored entry.  Needs R <= 16376 (4 * (R + 7)
+ *    fits in 16 bits for the kernel).
+ *  - CELTY_LAYOUT_INTERLEAVED (Section 4.2's offline interleave across
+ *    lanes): the RLC entries of every segment, cut into chunks of up to 64
+ *    groups (64 per chunk, the segment's last chunk holding the rest); within
+ *    a chunk of G_c groups, row-order entry e is stored in group e % G_c,
+ *    slot e / G_c, with its run (the runs keep their meaning).  Lane l of a
+ *    wavefront that loads the chunk's group l holds entries l, l + G_c, ...
+ *    Same arrays and sizes as CELTY_LAYOUT_RLC.
  */
 typedef struct celty_rlc_csc {
   int32_t version;          /* CELTY_FORMAT_VERSION */
@@ -87,10 +106,10 @@ typedef struct celty_rlc_csc {
   int64_t n_nnz;            /* stored values */
   int64_t n_pad;            /* padding entries */
   float max_abs;            /* largest |stored value| (0 if none) = the largest colmax; finite */
-  int32_t layout;           /* CELTY_LAYOUT_RLC */
+  int32_t layout;           /* CELTY_LAYOUT_RLC, _ROWS16 or _INTERLEAVED */
   const uint32_t* gptr;     /* [T*K + 1], 4-byte aligned */
   const uint16_t* values;   /* [8*G] fp16 bits, 16-byte aligned */
-  const uint32_t* runs;     /* [G], 4-byte aligned */
+  const uint32_t* runs;     /* [G] ([4*G] for ROWS16), 4-byte aligned (16 for ROWS16) */
   const uint16_t* colmax;   /* [K] fp16 bits, 4-byte aligned */
 } celty_rlc_csc;
 
@@ -100,11 +119,12 @@ typedef struct celty_rlc_csc {
  *   W      host, fp16 bit patterns, row-major M x K with row stride ldw >= K.
  *   mask   host, uint8 row-major with row stride ldm >= K; non-zero = kept.
  *          NULL keeps every entry (then only +-0 weights are dropped).
- *   R      tile height, 1 <= R; T = ceil(M/R).
- *   layout CELTY_LAYOUT_RLC.
- * Outputs (host, may not be NULL): n_groups, n_nnz, n_pad.
+ *   R      tile height, 1 <= R (<= 16376 for CELTY_LAYOUT_ROWS16); T = ceil(M/R).
+ *   layout CELTY_LAYOUT_RLC, CELTY_LAYOUT_ROWS16 or CELTY_LAYOUT_INTERLEAVED.
+ * Outputs (host, may not be NULL): n_groups, n_nnz, n_pad (0 for ROWS16).
  * Errors: EINVAL (null W or output pointer, M/K/R < 1, short stride, unknown
- *         layout), EOVERFLOW (n_groups > UINT32_MAX), ENOMEM.
+ *         layout, R too tall for ROWS16), EOVERFLOW (n_groups > UINT32_MAX),
+ *         ENOMEM.
  */
 celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm,
                                int32_t M, int32_t K, int32_t R, int32_t layout,
@@ -112,7 +132,8 @@ celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const uint8_t* ma
 
 /*
  * Encode into caller buffers (host): gptr [T*K+1], values [8*n_groups]
- * (16-byte aligned), runs [n_groups], colmax [K] (4-byte aligned).
+ * (16-byte aligned), runs [n_groups] ([4*n_groups], 16-byte aligned, for
+ * CELTY_LAYOUT_ROWS16), colmax [K] (4-byte aligned).
  * n_groups must equal the plan's value.  On success *out is filled (pointers
  * = the buffers given here, and max_abs = the largest magnitude among the
  * stored values).  n_threads: worker threads, 0 = all hardware threads.  The
@@ -129,10 +150,13 @@ celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8_t* mask, i
  * Decode a stream held in host memory back to dense form (host).
  *   W_out    host, M x K fp16 bits, row-major, stride K: stored values, +0 elsewhere.
  *   mask_out host, M x K uint8, stride K: 1 where a value is stored (may be NULL).
+ * Every layout is accepted; an interleaved stream is first put back in row
+ * order.
  * Errors: EINVAL (null pointers, bad header), EFORMAT (gptr not monotone from
  * 0 to n_groups, a stored value beyond its tile, an alignment entry with a
- * non-zero run, header counts, max_abs or colmax that disagree with the
- * stream).
+ * non-zero run (RLC) or another row than the last stored one (ROWS16),
+ * stored rows out of order (ROWS16), header counts, max_abs or colmax that
+ * disagree with the stream), ENOMEM.
  */
 celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out);
 
@@ -159,13 +183,19 @@ celty_status celty_select(const void* x, int32_t K, float tau, int32_t* idx, int
  * units), never more, and widened to fill two 8-wavefront workgroups per
  * unit evenly when the rounded width would load the units unevenly and the
  * slices stay heavy enough; one group per lane.  The K columns are cut into
- * ceil(K / cols_per_block) slices, at most 63 (the merge counts slices in one
- * byte of a 64-bit word).  A workgroup's lanes scan at most 8 columns each:
- * cols_per_block <= 512 * waves_per_block. */
+ * ceil(K / cols_per_block) slices, at most 63 (the merge counts 6-bit
+ * arrivals in a 64-bit word).  A workgroup's lanes scan at most 8 columns
+ * each: cols_per_block <= 512 * waves_per_block.
+ * lds_swizzle = 1 stores the LDS tile's row r at slot r ^ ((r >> 6) & 63)
+ * (an XOR swizzle against bank conflicts in the scatter-adds, Section 4.1;
+ * the result is the same).  It applies to CELTY_LAYOUT_RLC only.  The
+ * swizzle and the two other layouts run with one group per lane and one
+ * product per launch. */
 typedef struct celty_launch {
   int32_t cols_per_block;   /* columns of x one workgroup scans (1..4096) */
   int32_t waves_per_block;  /* 2, 4, 8 or 16 wavefronts of 64 lanes */
   int32_t groups_per_lane;  /* 1, 2 or 4 eight-entry groups per lane per pass */
+  int32_t lds_swizzle;      /* 0 (plain tile) or 1 (XOR-swizzled tile) */
 } celty_launch;
 
 /* A tile height R for encoding an M x K matrix for celty_spmspv (host only):
@@ -229,10 +259,13 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  * colmax must bound every |stored value| of its column (the encoder sets it
  * exactly): a smaller value can overflow the int32 tile and give wrong rows,
  * but never an access outside the arrays.
+ * Every layout gives the same y.
  * Errors: EINVAL (null or misaligned pointers, inconsistent header, NaN tau,
  *         non-finite or negative max_abs, short workspace, more than 63
  *         column slices, cols_per_block above 512 * waves_per_block,
- *         16 * n_groups >= 2^31), EHIP.
+ *         16 * n_groups >= 2^31, groups_per_lane > 1 with another layout
+ *         than RLC or with lds_swizzle, lds_swizzle with another layout),
+ *         EHIP.
  */
 celty_status celty_spmspv(const celty_rlc_csc* W, const void* x, float tau, void* y,
                           void* workspace, size_t workspace_bytes, void* stream);
@@ -260,8 +293,10 @@ celty_status celty_spmspv_ex(const celty_rlc_csc* W, const void* x, float tau, v
  *              the automatic choice is made per product, with 16 wavefronts
  *              when any product has R >= 1024.
  * Results are those of n separate celty_spmspv_ex calls with the same launch.
+ * With n > 1 every product must use CELTY_LAYOUT_RLC without lds_swizzle.
  * Errors: EINVAL (n outside 1..8, null arrays, any product's celty_spmspv
- *         error, overlapping buffers, short workspace), EHIP.
+ *         error, overlapping buffers, short workspace, another layout or
+ *         lds_swizzle with n > 1), EHIP.
  */
 celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const* W, const void* const* x,
                                 const float* tau, void* const* y, void* workspace,

@@ -43,7 +43,9 @@ CELTY_OK, CELTY_EINVAL, CELTY_ENOMEM, CELTY_EOVERFLOW, CELTY_EFORMAT, CELTY_EHIP
 FORMAT_VERSION = 2
 RUN_BITS = 4
 GROUP = 8
-LAYOUT_RLC = 0
+LAYOUT_RLC = 0           # 4-bit run lengths (the paper's format)
+LAYOUT_ROWS16 = 1        # 16-bit row offsets within the tile (decode-free)
+LAYOUT_INTERLEAVED = 2   # RLC entries in lane-interleaved order within chunks of 64 groups
 
 _p = ctypes.c_void_p
 _i32, _i64, _f32, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
@@ -57,7 +59,8 @@ class celty_rlc_csc(ctypes.Structure):
 
 
 class celty_launch(ctypes.Structure):
-    _fields_ = [("cols_per_block", _i32), ("waves_per_block", _i32), ("groups_per_lane", _i32)]
+    _fields_ = [("cols_per_block", _i32), ("waves_per_block", _i32), ("groups_per_lane", _i32),
+                ("lds_swizzle", _i32)]
 
 
 def _sig(name, res, *args):
@@ -170,7 +173,7 @@ def celty_encode(W: np.ndarray, mask, R: int, n_threads: int = 0, layout: int = 
     T = -(-M // int(R))
     gptr = _aligned_empty(T * K + 1, np.uint32)
     values = _aligned_empty(GROUP * G, np.uint16)
-    runs = _aligned_empty(G, np.uint32)
+    runs = _aligned_empty(4 * G if int(layout) == LAYOUT_ROWS16 else G, np.uint32)
     colmax = _aligned_empty(K, np.uint16)
     desc = celty_rlc_csc()
     _check(_encode(Wb.ctypes.data, K, None if m is None else m.ctypes.data, K, M, K, int(R), int(layout),
@@ -293,7 +296,8 @@ def _launch_struct(launch) -> Optional[celty_launch]:
         return launch
     cols, waves = launch[0], launch[1]
     groups = launch[2] if len(launch) > 2 else 0
-    return celty_launch(int(cols), int(waves), int(groups))
+    swizzle = launch[3] if len(launch) > 3 else 0
+    return celty_launch(int(cols), int(waves), int(groups), int(swizzle))
 
 
 def celty_spmspv(W: DeviceRlcCsc, x, tau: float, y, workspace, stream=None) -> None:
@@ -364,7 +368,8 @@ def celty_spmspv_plan(W, launch=None) -> dict:
     _check(_plan(ctypes.byref(d), None if ls is None else ctypes.byref(ls), ctypes.byref(out),
                  ctypes.byref(nb), ctypes.byref(lds)), "celty_spmspv_plan")
     return dict(cols_per_block=out.cols_per_block, waves_per_block=out.waves_per_block,
-                groups_per_lane=out.groups_per_lane, blocks=nb.value, lds_bytes=lds.value)
+                groups_per_lane=out.groups_per_lane, lds_swizzle=out.lds_swizzle, blocks=nb.value,
+                lds_bytes=lds.value)
 
 
 def default_tile_rows(M: int, K: int) -> int:
@@ -373,7 +378,7 @@ def default_tile_rows(M: int, K: int) -> int:
 
 
 __all__ = [
-    "FORMAT_VERSION", "LAYOUT_RLC", "default_tile_rows",
+    "FORMAT_VERSION", "LAYOUT_RLC", "LAYOUT_ROWS16", "LAYOUT_INTERLEAVED", "default_tile_rows",
     "celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv", "celty_spmspv_ex",
     "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "new_batch_workspace", "celty_spmspv_noalloc",
     "celty_spmspv_plan", "celty_spmspv_workspace_bytes", "celty_spmspv_workspace_init", "celty_status_string",

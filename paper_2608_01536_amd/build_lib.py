@@ -20,8 +20,9 @@ FLAGS = [
     # packed fp32 VALU forms stay off (the compiler must not emit v_pk_*_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # the leading kernel arguments (those a workgroup's prologue needs: the
-    # selection's pointers and sizes, the LDS layout, max|w|, R and M; 14
-    # scalar registers) are preloaded at dispatch instead of fetched from memory
+    # selection's pointers and sizes, the column maxima, R and M; nine
+    # arguments in 12 scalar registers) are preloaded at dispatch instead of
+    # fetched from memory
     "-Xarch_device", "-mllvm=-amdgpu-kernarg-preload-count=13",
     "-I", os.path.join(ROOT, "include"), "-pthread",
 ]

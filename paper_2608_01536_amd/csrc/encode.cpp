@@ -5,6 +5,12 @@
 // mask are read row-major and contiguously.  Segments of one item are
 // contiguous in the tile-major layout, so items never write the same bytes
 // and the output does not depend on the thread count.
+//
+// Three layouts of the rows: 4-bit runs (the paper's); 16-bit row offsets
+// within the tile (no padding entries, a decode-free form); and the RLC
+// entries of each segment in lane-interleaved order within chunks of up to
+// 64 groups (Section 4.2), produced by permuting each item's segments after
+// the RLC fill.
 
 #include <algorithm>
 #include <atomic>
@@ -19,6 +25,8 @@ namespace {
 
 constexpr int kCap = (1 << CELTY_RUN_BITS) - 1;   // largest run a padding entry carries
 constexpr int kColBlock = 512;                      // columns per work item
+constexpr int kChunk = 64;                          // groups per interleave chunk (a wavefront's lanes)
+constexpr int32_t kMaxRows16 = 16376;               // tile rows of ROWS16: 4 * (R + 7) fits in 16 bits
 
 inline bool stored(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm, int64_t r,
                    int64_t k) {
@@ -63,15 +71,23 @@ std::vector<Item> make_items(int32_t T, int32_t K) {
 }
 
 // Runs fn(item_index) over all items on n_threads workers.  Returns false if
-// a worker could not be started (the caller maps this to ENOMEM).
+// a worker could not be started or an item threw (its scratch could not be
+// allocated); the caller maps this to ENOMEM.  No exception leaves a worker.
 template <class Fn>
 bool parallel_items(size_t n_items, int32_t n_threads, Fn fn) {
   unsigned hw = std::thread::hardware_concurrency();
   size_t nt = n_threads > 0 ? size_t(n_threads) : size_t(hw ? hw : 1);
   nt = std::max<size_t>(1, std::min(nt, n_items));
   std::atomic<size_t> next{0};
+  std::atomic<bool> failed{false};
   auto worker = [&]() {
-    for (size_t i = next.fetch_add(1); i < n_items; i = next.fetch_add(1)) fn(i);
+    for (size_t i = next.fetch_add(1); i < n_items; i = next.fetch_add(1)) {
+      try {
+        fn(i);
+      } catch (...) {
+        failed.store(true);
+      }
+    }
   };
   std::vector<std::thread> pool;
   try {
@@ -82,13 +98,13 @@ bool parallel_items(size_t n_items, int32_t n_threads, Fn fn) {
   }
   worker();
   for (auto& th : pool) th.join();
-  return true;
+  return !failed.load();
 }
 
 // Counts entries per segment of one item; writes groups per segment into
 // seg_groups (indexed s - (t*K + k0)) when non-null and adds the totals.
 void count_item(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm, int32_t M,
-                int32_t R, const Item& it, std::vector<int32_t>& last, std::vector<int64_t>& cnt,
+                int32_t R, bool bridge, const Item& it, std::vector<int32_t>& last, std::vector<int64_t>& cnt,
                 int64_t& nnz, int64_t& pad, int64_t& groups, uint32_t* seg_groups) {
   const int32_t nk = it.k1 - it.k0;
   const int64_t r0 = int64_t(it.t) * R, r1 = std::min<int64_t>(M, r0 + R);
@@ -98,9 +114,9 @@ void count_item(const uint16_t* W, int64_t ldw, const uint8_t* mask, int64_t ldm
     const int32_t rel = int32_t(r - r0);
     for (int32_t j = 0; j < nk; ++j) {
       if (!stored(W, ldw, mask, ldm, r, it.k0 + j)) continue;
-      const int32_t gap = rel - last[j] - 1;
-      cnt[j] += gap / (kCap + 1) + 1;
-      pad += gap / (kCap + 1);
+      const int32_t np = bridge ? (rel - last[j] - 1) / (kCap + 1) : 0;   // padding entries before it
+      cnt[j] += np + 1;
+      pad += np;
       ++nnz;
       last[j] = rel;
     }
@@ -116,8 +132,33 @@ celty_status check_common(const uint16_t* W, int64_t ldw, const uint8_t* mask, i
                           int32_t M, int32_t K, int32_t R, int32_t layout) {
   if (!W || M < 1 || K < 1 || R < 1 || ldw < K) return CELTY_EINVAL;
   if (mask && ldm < K) return CELTY_EINVAL;
-  if (layout != CELTY_LAYOUT_RLC) return CELTY_EINVAL;
+  if (layout != CELTY_LAYOUT_RLC && layout != CELTY_LAYOUT_ROWS16 && layout != CELTY_LAYOUT_INTERLEAVED)
+    return CELTY_EINVAL;
+  if (layout == CELTY_LAYOUT_ROWS16 && R > kMaxRows16) return CELTY_EINVAL;
   return CELTY_OK;
+}
+
+// Lane-interleaved order of one segment's n groups (entries in row order in
+// values[0 .. 8n) and the packed runs[0 .. n)): within each chunk of
+// gc <= 64 groups, row-order entry e moves to group e % gc, slot e / gc
+// (inverse = true moves it back).  tv and tr are scratch of 8 * 64 entries.
+void interleave_segment(uint16_t* values, uint32_t* runs, int64_t n, bool inverse, uint16_t* tv, uint8_t* tr) {
+  for (int64_t c0 = 0; c0 < n; c0 += kChunk) {
+    const int64_t gc = std::min<int64_t>(kChunk, n - c0);
+    uint16_t* v = values + c0 * CELTY_GROUP;
+    uint32_t* r = runs + c0;
+    for (int64_t e = 0; e < gc * CELTY_GROUP; ++e) {
+      tv[e] = v[e];
+      tr[e] = uint8_t((r[e / CELTY_GROUP] >> (4 * (e % CELTY_GROUP))) & 0xFu);
+    }
+    std::fill(r, r + gc, 0u);
+    for (int64_t e = 0; e < gc * CELTY_GROUP; ++e) {
+      const int64_t stored = (e % gc) * CELTY_GROUP + e / gc;   // group e % gc, slot e / gc
+      const int64_t from = inverse ? stored : e, to = inverse ? e : stored;
+      v[to] = tv[from];
+      r[to / CELTY_GROUP] |= uint32_t(tr[from]) << (4 * (to % CELTY_GROUP));
+    }
+  }
 }
 
 }  // namespace
@@ -135,7 +176,7 @@ extern "C" celty_status celty_encode_plan(const uint16_t* W, int64_t ldw, const 
       std::vector<int32_t> last(kColBlock);
       std::vector<int64_t> cnt(kColBlock);
       int64_t a = 0, b = 0, c = 0;
-      count_item(W, ldw, mask, ldm, M, R, items[i], last, cnt, a, b, c, nullptr);
+      count_item(W, ldw, mask, ldm, M, R, layout != CELTY_LAYOUT_ROWS16, items[i], last, cnt, a, b, c, nullptr);
       nnz[i] = a;
       pad[i] = b;
       grp[i] = c;
@@ -166,7 +207,8 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
   if (celty_status st = check_common(W, ldw, mask, ldm, M, K, R, layout)) return st;
   if (!gptr || !out || !colmax || n_threads < 0 || n_groups < 0) return CELTY_EINVAL;
   if (n_groups > 0 && (!values || !runs)) return CELTY_EINVAL;
-  if ((reinterpret_cast<uintptr_t>(values) & 15u) || (reinterpret_cast<uintptr_t>(runs) & 3u) ||
+  const bool rows16 = layout == CELTY_LAYOUT_ROWS16;
+  if ((reinterpret_cast<uintptr_t>(values) & 15u) || (reinterpret_cast<uintptr_t>(runs) & (rows16 ? 15u : 3u)) ||
       (reinterpret_cast<uintptr_t>(gptr) & 3u) || (reinterpret_cast<uintptr_t>(colmax) & 3u))
     return CELTY_EINVAL;
   if (n_groups > int64_t(UINT32_MAX)) return CELTY_EOVERFLOW;
@@ -185,7 +227,7 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
       std::vector<int32_t> last(kColBlock);
       std::vector<int64_t> cnt(kColBlock);
       int64_t a = 0, b = 0, c = 0;
-      count_item(W, ldw, mask, ldm, M, R, it, last, cnt, a, b, c, gptr + int64_t(it.t) * K + it.k0);
+      count_item(W, ldw, mask, ldm, M, R, !rows16, it, last, cnt, a, b, c, gptr + int64_t(it.t) * K + it.k0);
       nnz[i] = a;
       pad[i] = b;
     });
@@ -206,8 +248,10 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
       const int32_t nk = it.k1 - it.k0;
       const int64_t sbase = int64_t(it.t) * K + it.k0;
       const int64_t g0 = gptr[sbase], g1 = gptr[sbase + nk];
+      const int64_t run_words = rows16 ? 4 : 1;   // words of row information per group
       std::memset(values + g0 * CELTY_GROUP, 0, size_t(g1 - g0) * CELTY_GROUP * sizeof(uint16_t));
-      std::memset(runs + g0, 0, size_t(g1 - g0) * sizeof(uint32_t));
+      std::memset(runs + g0 * run_words, 0, size_t(g1 - g0) * run_words * sizeof(uint32_t));
+      uint16_t* rows = reinterpret_cast<uint16_t*>(runs);   // ROWS16: entry e's offset at rows[e]
       std::vector<int32_t> last(nk, -1);
       std::vector<int64_t> pos(nk);   // next entry index (absolute) of each segment
       for (int32_t j = 0; j < nk; ++j) pos[j] = int64_t(gptr[sbase + j]) * CELTY_GROUP;
@@ -221,19 +265,38 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
         const int32_t rel = int32_t(r - r0);
         for (int32_t j = 0; j < nk; ++j) {
           if (!stored(W, ldw, mask, ldm, r, it.k0 + j)) continue;
-          int32_t gap = rel - last[j] - 1;
-          while (gap > kCap) {          // padding first, carrying the largest run
-            emit(j, 0, uint32_t(kCap));
-            gap -= kCap + 1;
-          }
           const uint16_t v = W[r * ldw + it.k0 + j];
-          emit(j, v, uint32_t(gap));
+          if (rows16) {
+            const int64_t e = pos[j]++;
+            values[e] = v;
+            rows[e] = uint16_t(rel);
+          } else {
+            int32_t gap = rel - last[j] - 1;
+            while (gap > kCap) {          // padding first, carrying the largest run
+              emit(j, 0, uint32_t(kCap));
+              gap -= kCap + 1;
+            }
+            emit(j, v, uint32_t(gap));
+          }
           uint16_t& cm = tile_colmax[size_t(sbase + j)];
           cm = std::max<uint16_t>(cm, uint16_t(v & 0x7FFFu));   // magnitude bits order like the values
           last[j] = rel;
         }
       }
-      // alignment entries (0, 0) are already in place from the memset
+      // alignment entries: (0, 0) from the memset for runs; for row offsets,
+      // value 0 at the segment's last stored row
+      if (rows16) {
+        for (int32_t j = 0; j < nk; ++j)
+          for (int64_t e = pos[j]; e < int64_t(gptr[sbase + j + 1]) * CELTY_GROUP; ++e) rows[e] = uint16_t(last[j]);
+      }
+      if (layout == CELTY_LAYOUT_INTERLEAVED) {
+        std::vector<uint16_t> tv(kChunk * CELTY_GROUP);
+        std::vector<uint8_t> tr(kChunk * CELTY_GROUP);
+        for (int32_t j = 0; j < nk; ++j) {
+          const int64_t a = gptr[sbase + j], b = gptr[sbase + j + 1];
+          interleave_segment(values + a * CELTY_GROUP, runs + a, b - a, false, tv.data(), tr.data());
+        }
+      }
     });
     if (!ok) return CELTY_ENOMEM;
 
@@ -271,40 +334,25 @@ extern "C" celty_status celty_encode(const uint16_t* W, int64_t ldw, const uint8
   }
 }
 
-extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out) {
-  if (!enc || !W_out) return CELTY_EINVAL;
-  if (enc->version != CELTY_FORMAT_VERSION || enc->run_bits != CELTY_RUN_BITS) return CELTY_EINVAL;
-  if (enc->layout != CELTY_LAYOUT_RLC) return CELTY_EINVAL;
-  const int32_t M = enc->M, K = enc->K, R = enc->R, T = enc->T;
-  if (M < 1 || K < 1 || R < 1 || T != int32_t((int64_t(M) + R - 1) / R) || enc->n_groups < 0)
-    return CELTY_EINVAL;
-  if (!enc->gptr || !enc->colmax || (enc->n_groups > 0 && (!enc->values || !enc->runs))) return CELTY_EINVAL;
-  const int64_t nseg = int64_t(T) * K;
-  const uint32_t* gptr = enc->gptr;
-  if (gptr[0] != 0 || int64_t(gptr[nseg]) != enc->n_groups) return CELTY_EFORMAT;
-  for (int64_t s = 0; s < nseg; ++s)
-    if (gptr[s + 1] < gptr[s]) return CELTY_EFORMAT;
-  std::memset(W_out, 0, size_t(M) * K * sizeof(uint16_t));
-  if (mask_out) std::memset(mask_out, 0, size_t(M) * K);
-  int64_t nnz = 0, pad = 0;
-  uint16_t mbits = 0;
-  std::vector<uint16_t> cmax;
-  try {
-    cmax.assign(size_t(K), 0);
-  } catch (...) {
-    return CELTY_ENOMEM;
-  }
+namespace {
+
+// Decodes the RLC entries of every segment (row order) into W_out/mask_out
+// and the counts; EFORMAT on a malformed stream.
+celty_status decode_rlc(const celty_rlc_csc* enc, const uint16_t* values, const uint32_t* runs, uint16_t* W_out,
+                        uint8_t* mask_out, int64_t& nnz, int64_t& pad, std::vector<uint16_t>& cmax) {
+  const int32_t M = enc->M, K = enc->K, R = enc->R;
+  const int64_t nseg = int64_t(enc->T) * K;
   for (int64_t s = 0; s < nseg; ++s) {
     const int64_t t = s / K, k = s % K;
     const int64_t hi = std::min<int64_t>(M, (t + 1) * int64_t(R));
     int64_t row = t * int64_t(R) - 1;
-    int64_t e0 = int64_t(gptr[s]) * CELTY_GROUP, e1 = int64_t(gptr[s + 1]) * CELTY_GROUP;
+    const int64_t e0 = int64_t(enc->gptr[s]) * CELTY_GROUP, e1 = int64_t(enc->gptr[s + 1]) * CELTY_GROUP;
     int64_t last_real = e0 - 1;
     for (int64_t e = e0; e < e1; ++e)
-      if (enc->values[e] & 0x7FFFu) last_real = e;
+      if (values[e] & 0x7FFFu) last_real = e;
     for (int64_t e = e0; e < e1; ++e) {
-      const uint32_t run = (enc->runs[e / CELTY_GROUP] >> (4 * (e % CELTY_GROUP))) & 0xFu;
-      const uint16_t v = enc->values[e];
+      const uint32_t run = (runs[e / CELTY_GROUP] >> (4 * (e % CELTY_GROUP))) & 0xFu;
+      const uint16_t v = values[e];
       row += int64_t(run) + 1;
       if (e > last_real) {            // alignment entries must be (0, 0)
         if (run != 0 || v != 0) return CELTY_EFORMAT;
@@ -314,7 +362,6 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
         if (row >= hi) return CELTY_EFORMAT;
         W_out[row * K + k] = v;
         if (mask_out) mask_out[row * K + k] = 1;
-        mbits = std::max<uint16_t>(mbits, uint16_t(v & 0x7FFFu));
         cmax[size_t(k)] = std::max<uint16_t>(cmax[size_t(k)], uint16_t(v & 0x7FFFu));
         ++nnz;
       } else {
@@ -322,9 +369,94 @@ extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, 
       }
     }
   }
+  return CELTY_OK;
+}
+
+// Row offsets: stored values in strictly increasing rows inside the tile,
+// then alignment entries (0, the last stored offset).
+celty_status decode_rows16(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out, int64_t& nnz,
+                           std::vector<uint16_t>& cmax) {
+  const int32_t M = enc->M, K = enc->K, R = enc->R;
+  const int64_t nseg = int64_t(enc->T) * K;
+  const uint16_t* rows = reinterpret_cast<const uint16_t*>(enc->runs);
+  for (int64_t s = 0; s < nseg; ++s) {
+    const int64_t t = s / K, k = s % K;
+    const int64_t hi = std::min<int64_t>(M, (t + 1) * int64_t(R)) - t * int64_t(R);
+    const int64_t e0 = int64_t(enc->gptr[s]) * CELTY_GROUP, e1 = int64_t(enc->gptr[s + 1]) * CELTY_GROUP;
+    int64_t prev = -1;
+    bool tail = false;
+    for (int64_t e = e0; e < e1; ++e) {
+      const uint16_t v = enc->values[e];
+      const int64_t r = rows[e];
+      if (v & 0x7FFFu) {
+        if (tail || r >= hi || r <= prev) return CELTY_EFORMAT;
+        W_out[(t * int64_t(R) + r) * K + k] = v;
+        if (mask_out) mask_out[(t * int64_t(R) + r) * K + k] = 1;
+        cmax[size_t(k)] = std::max<uint16_t>(cmax[size_t(k)], uint16_t(v & 0x7FFFu));
+        ++nnz;
+        prev = r;
+      } else {
+        if (v != 0 || prev < 0 || r != prev) return CELTY_EFORMAT;
+        tail = true;
+      }
+    }
+  }
+  return CELTY_OK;
+}
+
+}  // namespace
+
+extern "C" celty_status celty_decode(const celty_rlc_csc* enc, uint16_t* W_out, uint8_t* mask_out) {
+  if (!enc || !W_out) return CELTY_EINVAL;
+  if (enc->version != CELTY_FORMAT_VERSION || enc->run_bits != CELTY_RUN_BITS) return CELTY_EINVAL;
+  const int32_t layout = enc->layout;
+  if (layout != CELTY_LAYOUT_RLC && layout != CELTY_LAYOUT_ROWS16 && layout != CELTY_LAYOUT_INTERLEAVED)
+    return CELTY_EINVAL;
+  const int32_t M = enc->M, K = enc->K, R = enc->R, T = enc->T;
+  if (M < 1 || K < 1 || R < 1 || T != int32_t((int64_t(M) + R - 1) / R) || enc->n_groups < 0)
+    return CELTY_EINVAL;
+  if (layout == CELTY_LAYOUT_ROWS16 && R > kMaxRows16) return CELTY_EINVAL;
+  if (!enc->gptr || !enc->colmax || (enc->n_groups > 0 && (!enc->values || !enc->runs))) return CELTY_EINVAL;
+  const int64_t nseg = int64_t(T) * K;
+  const uint32_t* gptr = enc->gptr;
+  if (gptr[0] != 0 || int64_t(gptr[nseg]) != enc->n_groups) return CELTY_EFORMAT;
+  for (int64_t s = 0; s < nseg; ++s)
+    if (gptr[s + 1] < gptr[s]) return CELTY_EFORMAT;
+  std::memset(W_out, 0, size_t(M) * K * sizeof(uint16_t));
+  if (mask_out) std::memset(mask_out, 0, size_t(M) * K);
+  int64_t nnz = 0, pad = 0;
+  std::vector<uint16_t> cmax;
+  std::vector<uint16_t> dv;   // an interleaved stream put back in row order
+  std::vector<uint32_t> dr;
+  try {
+    cmax.assign(size_t(K), 0);
+    if (layout == CELTY_LAYOUT_INTERLEAVED) {
+      dv.assign(enc->values, enc->values + enc->n_groups * CELTY_GROUP);
+      dr.assign(enc->runs, enc->runs + enc->n_groups);
+    }
+  } catch (...) {
+    return CELTY_ENOMEM;
+  }
+  celty_status st;
+  if (layout == CELTY_LAYOUT_ROWS16) {
+    st = decode_rows16(enc, W_out, mask_out, nnz, cmax);
+  } else if (layout == CELTY_LAYOUT_INTERLEAVED) {
+    uint16_t tv[kChunk * CELTY_GROUP];
+    uint8_t tr[kChunk * CELTY_GROUP];
+    for (int64_t s = 0; s < nseg; ++s)
+      interleave_segment(dv.data() + int64_t(gptr[s]) * CELTY_GROUP, dr.data() + gptr[s], gptr[s + 1] - gptr[s],
+                         true, tv, tr);
+    st = decode_rlc(enc, dv.data(), dr.data(), W_out, mask_out, nnz, pad, cmax);
+  } else {
+    st = decode_rlc(enc, enc->values, enc->runs, W_out, mask_out, nnz, pad, cmax);
+  }
+  if (st != CELTY_OK) return st;
   if (nnz != enc->n_nnz || pad != enc->n_pad || nnz + pad != enc->n_entries) return CELTY_EFORMAT;
-  if (enc->max_abs != half_bits_to_float(mbits)) return CELTY_EFORMAT;
-  for (int32_t k = 0; k < K; ++k)
+  uint16_t mbits = 0;
+  for (int32_t k = 0; k < K; ++k) {
     if (enc->colmax[k] != cmax[size_t(k)]) return CELTY_EFORMAT;
+    mbits = std::max(mbits, cmax[size_t(k)]);
+  }
+  if (enc->max_abs != half_bits_to_float(mbits)) return CELTY_EFORMAT;
   return CELTY_OK;
 }

@@ -63,21 +63,39 @@ constexpr unsigned long long kTicketCount = 1ull << 58;
 // buffer loads), so the streamed weights do not displace cached lines.
 constexpr int kStreamPolicy = 2;
 
+// Kernel variants: the row encodings of the format (layout field) and the
+// LDS tile's slot order.
+constexpr int kVarRlc = 0;           // 4-bit runs, plain tile
+constexpr int kVarSwizzle = 1;       // 4-bit runs, tile row r at slot r ^ ((r >> 6) & 63)
+constexpr int kVarRows16 = 2;        // 16-bit row offsets
+constexpr int kVarInterleaved = 3;   // 4-bit runs in lane-interleaved order within chunks of 64 groups
+constexpr int kChunk = 64;           // groups per interleave chunk
+
 // Dynamic LDS of a workgroup (byte offsets; the int32 tile is at 0): the
 // tile of R rows plus 7 alignment rows and 128 rows of slack that bound where
 // a corrupt stream could write (a group base is capped at R + 7 and a group
-// adds at most 128); the selection's list of Kc segments; the walk's scratch
-// (64 * G ints per wavefront); the block scan's per-wavefront totals (3 words
-// each).  The host sizes the launch with the same function.
+// adds at most 128), rounded up to 64 rows so that the swizzled slot order
+// (a permutation within aligned blocks of 64 rows) stays inside it; the
+// selection's list of Kc segments; the walk's scratch (64 * scr_words ints
+// per wavefront); the block scan's per-wavefront totals (3 words each).  The
+// host sizes the launch with the same function.
 struct LdsLayout {
   int tile_slots, seg_off, scr_off, misc_off, bytes;
 };
 __host__ __device__ constexpr int align16(int v) { return (v + 15) & ~15; }
-__host__ __device__ constexpr LdsLayout lds_layout(int R, int Kc, int waves, int groups) {
-  return LdsLayout{R + kSlack, align16(4 * (R + kSlack)), align16(4 * (R + kSlack)) + 16 * Kc,
-                   align16(4 * (R + kSlack)) + 16 * Kc + 256 * waves * groups,
-                   align16(align16(4 * (R + kSlack)) + 16 * Kc + 256 * waves * groups + 12 * waves)};
+__host__ __device__ constexpr int tile_slots_of(int R) { return (R + kSlack + 63) & ~63; }
+__host__ __device__ constexpr LdsLayout lds_layout(int R, int Kc, int waves, int scr_words) {
+  return LdsLayout{tile_slots_of(R), 4 * tile_slots_of(R), 4 * tile_slots_of(R) + 16 * Kc,
+                   4 * tile_slots_of(R) + 16 * Kc + 256 * waves * scr_words,
+                   align16(4 * tile_slots_of(R) + 16 * Kc + 256 * waves * scr_words + 12 * waves)};
 }
+// Scratch ints per lane of the walk: one per group of a pass, four for the
+// interleaved layout's packed per-slot scans.
+__host__ __device__ constexpr int scr_words_of(int groups, int var) { return var == kVarInterleaved ? 4 : groups; }
+
+// Tile slot of row r (as a byte offset, 4 * r) in the swizzled order:
+// r ^ ((r >> 6) & 63), a permutation within each aligned block of 64 rows.
+__device__ __forceinline__ uint32_t swizzle4(uint32_t a) { return a ^ ((a >> 6) & 0xFCu); }
 
 struct SegInfo {
   uint32_t gstart;   // first group of the segment in the values/runs arrays
@@ -243,12 +261,13 @@ struct Streams {
   __amdgpu_buffer_rsrc_t runs;
 };
 
-__device__ __forceinline__ Streams make_streams(const uint4* values, const uint32_t* runs, uint32_t n_groups) {
+__device__ __forceinline__ Streams make_streams(const uint4* values, const uint32_t* runs, uint32_t n_groups,
+                                                uint32_t run_bytes) {
   Streams st;
   st.values = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(values), static_cast<short>(0),
                                                 static_cast<int>(n_groups * 16u), 0x00020000);
   st.runs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(runs), static_cast<short>(0),
-                                              static_cast<int>(n_groups * 4u), 0x00020000);
+                                              static_cast<int>(n_groups * run_bytes), 0x00020000);
   return st;
 }
 
@@ -258,6 +277,7 @@ template <int G>
 struct Pass {
   uint4 v[G];        // 8 fp16 values per group
   uint32_t rw[G];    // 8 packed 4-bit runs per group
+  uint4 rr[G];       // 8 16-bit row offsets per group (16-bit row layout)
   int hpos[G];       // flat position of the group's segment head relative to the pass start (< 0: earlier)
   float xs[G];       // scaled x_k of the group's column
   uint32_t live;     // bit i: group i holds data
@@ -271,7 +291,7 @@ struct Pass {
 // assignment and has every lane idle.  scr holds 64*G ints per wavefront:
 // segment heads are tagged with a negative value unique to the pass (the
 // accumulation step stores non-negative prefix sums in the same array).
-template <int G>
+template <int G, bool ROWS16>
 __device__ __forceinline__ void fetch_pass(Pass<G>& a, const Streams& st, const SegInfo* seg, int* scr,
                                            uint32_t pb, int icur, int i_end, uint32_t pe, int lane) {
   constexpr uint32_t P = kWave * G;
@@ -332,7 +352,12 @@ __device__ __forceinline__ void fetch_pass(Pass<G>& a, const Streams& st, const 
   for (int i = 0; i < G; ++i) {
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(st.values, static_cast<int>(gl[i] << 4), 0, kStreamPolicy);
     a.v[i] = make_uint4(v[0], v[1], v[2], v[3]);
-    a.rw[i] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>(gl[i] << 2), 0, 0);
+    if constexpr (ROWS16) {
+      const auto r = __builtin_amdgcn_raw_buffer_load_b128(st.runs, static_cast<int>(gl[i] << 4), 0, kStreamPolicy);
+      a.rr[i] = make_uint4(r[0], r[1], r[2], r[3]);
+    } else {
+      a.rw[i] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>(gl[i] << 2), 0, 0);
+    }
   }
 }
 
@@ -370,6 +395,30 @@ template <int J>
 __device__ __forceinline__ void tile_add(uint32_t a, int v) {
   asm volatile("ds_add_u32 %0, %1 offset:%2" : : "v"(a), "v"(v), "i"(4 * (J + 1)) : "memory");
 }
+// The same at LDS byte address a exactly.
+__device__ __forceinline__ void tile_add_at(uint32_t a, int v) {
+  asm volatile("ds_add_u32 %0, %1" : : "v"(a), "v"(v) : "memory");
+}
+
+// a + the 16-bit half Q of b in one VALU operation (SDWA source select).
+template <int Q>
+__device__ __forceinline__ uint32_t add_word(uint32_t a, uint32_t b) {
+  uint32_t r;
+  if constexpr (Q == 0)
+    asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0"
+        : "=v"(r) : "v"(a), "v"(b));
+  else
+    asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_1"
+        : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Both 16-bit halves of w, each clamped to the halves of c.
+__device__ __forceinline__ uint32_t min_u16x2(uint32_t w, uint32_t c) {
+  uint32_t r;
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(r) : "v"(w), "v"(c));
+  return r;
+}
 
 // Decodes one pass and adds its products into the fixed-point tile at LDS
 // byte address tile_lds.  Row arithmetic is done on byte offsets, 4 * row: a
@@ -378,7 +427,7 @@ __device__ __forceinline__ void tile_add(uint32_t a, int v) {
 // constant 4 * (j + 1) is an immediate.  Returns the
 // segment-relative sum of 4 * (run + 1) through lane 63's last group (the
 // carry when that segment goes on into the next pass), wavefront-uniform.
-template <int G>
+template <int G, bool SWZ>
 __device__ __forceinline__ int accumulate_pass(const Pass<G>& a, int carry4, int base4_cap, uint32_t tile_lds,
                                                int* scr, int lane) {
   uint32_t R4e[G], R4o[G];
@@ -409,8 +458,33 @@ __device__ __forceinline__ int accumulate_pass(const Pass<G>& a, int carry4, int
     const int rel4 = a.hpos[i] >= 0 ? Y - at_head : Y + carry4;   // segment-relative
     // entry j lands at base4 + sum_{i<=j} 4 r_i + 4 (j + 1) with base4 >= -4;
     // the cap keeps even a corrupt stream inside the tile's slack
-    const uint32_t base4 = static_cast<uint32_t>(min(rel4 - 4, base4_cap)) + tile_lds;
-    if ((a.live >> i) & 1u) {
+    const uint32_t base4 = static_cast<uint32_t>(min(rel4 - 4, base4_cap)) + (SWZ ? 0u : tile_lds);
+    if constexpr (SWZ) {
+      if ((a.live >> i) & 1u) {
+        // the running offset is tile-relative and advances by 4 (r_j + 1)
+        // (each byte at most 64, so adding 4 per byte cannot carry); the
+        // slot order is applied to it, then the tile's address added
+        const float xs = a.xs[i];
+        const uint32_t E = R4e[i] + 0x04040404u, O = R4o[i] + 0x04040404u;
+        uint32_t ad = base4;
+        ad = add_byte<0>(ad, E);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_lo_f16(a.v[i].x, xs)));
+        ad = add_byte<0>(ad, O);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_hi_f16(a.v[i].x, xs)));
+        ad = add_byte<1>(ad, E);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_lo_f16(a.v[i].y, xs)));
+        ad = add_byte<1>(ad, O);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_hi_f16(a.v[i].y, xs)));
+        ad = add_byte<2>(ad, E);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_lo_f16(a.v[i].z, xs)));
+        ad = add_byte<2>(ad, O);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_hi_f16(a.v[i].z, xs)));
+        ad = add_byte<3>(ad, E);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_lo_f16(a.v[i].w, xs)));
+        ad = add_byte<3>(ad, O);
+        tile_add_at(swizzle4(ad) + tile_lds, round_to_fixed(mul_hi_f16(a.v[i].w, xs)));
+      }
+    } else if ((a.live >> i) & 1u) {
       const float xs = a.xs[i];
       uint32_t ad = base4;
       ad = add_byte<0>(ad, R4e[i]);
@@ -433,6 +507,168 @@ __device__ __forceinline__ int accumulate_pass(const Pass<G>& a, int carry4, int
     if (i == G - 1) tail = rel4 + S4[i];
   }
   return __builtin_amdgcn_readlane(tail, kWave - 1);
+}
+
+// 16-bit row layout: each entry's row offset is loaded, so there is nothing
+// to reconstruct.  Offsets are clamped to R + 7 (the tile's slack), four
+// times each (4 * (R + 7) < 2^16), and added to the tile's address per entry.
+template <int G>
+__device__ __forceinline__ void accumulate_pass_rows16(const Pass<G>& a, uint32_t cap_rows2, uint32_t tile_lds) {
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    if ((a.live >> i) & 1u) {
+      const float xs = a.xs[i];
+      const uint32_t r0 = min_u16x2(a.rr[i].x, cap_rows2) << 2, r1 = min_u16x2(a.rr[i].y, cap_rows2) << 2;
+      const uint32_t r2 = min_u16x2(a.rr[i].z, cap_rows2) << 2, r3 = min_u16x2(a.rr[i].w, cap_rows2) << 2;
+      tile_add_at(add_word<0>(tile_lds, r0), round_to_fixed(mul_lo_f16(a.v[i].x, xs)));
+      tile_add_at(add_word<1>(tile_lds, r0), round_to_fixed(mul_hi_f16(a.v[i].x, xs)));
+      tile_add_at(add_word<0>(tile_lds, r1), round_to_fixed(mul_lo_f16(a.v[i].y, xs)));
+      tile_add_at(add_word<1>(tile_lds, r1), round_to_fixed(mul_hi_f16(a.v[i].y, xs)));
+      tile_add_at(add_word<0>(tile_lds, r2), round_to_fixed(mul_lo_f16(a.v[i].z, xs)));
+      tile_add_at(add_word<1>(tile_lds, r2), round_to_fixed(mul_hi_f16(a.v[i].z, xs)));
+      tile_add_at(add_word<0>(tile_lds, r3), round_to_fixed(mul_lo_f16(a.v[i].w, xs)));
+      tile_add_at(add_word<1>(tile_lds, r3), round_to_fixed(mul_hi_f16(a.v[i].w, xs)));
+    }
+  }
+}
+
+// ---- interleaved layout ---------------------------------------------------
+// A pass holds whole chunks only: a chunk's eight slots are consecutive runs
+// of the row order across its lanes, so decoding slot j needs the runs of
+// every lane of the chunk.  The wavefront's range and its passes are cut at
+// chunk boundaries: at a segment's head and every 64 groups after it, and
+// at its end.
+
+// The first chunk boundary at or after flat group `at` (wavefront-uniform).
+__device__ __forceinline__ uint32_t chunk_boundary(const SegInfo* seg, int n_seg, uint32_t n_grp, uint32_t at,
+                                                   int lane) {
+  if (at >= n_grp) return n_grp;
+  SegInfo s;
+  holding_segment(seg, n_seg, at, lane, s);
+  const uint32_t b = s.off + ((at - s.off + static_cast<uint32_t>(kChunk - 1)) & ~static_cast<uint32_t>(kChunk - 1));
+  return min(b, s.off + s.cnt);
+}
+
+struct PassIl {
+  uint4 v;           // 8 fp16 values (slots 0..7)
+  uint32_t rw;       // their 8 packed 4-bit runs
+  float xs;          // scaled x_k of the group's column
+  int hl, el;        // lanes of the group's chunk head and last group, within the pass
+  bool first;        // the chunk is its segment's first (else it goes on from the previous pass, at lane 0)
+  bool live;
+  uint32_t pend;     // flat end of the pass (wavefront-uniform)
+  int next_seg;      // segment holding pend (wavefront-uniform)
+  bool cont;         // the segment of the pass's last chunk goes on past pend (wavefront-uniform)
+};
+
+// Assigns the chunks that fit whole in [pb, min(pb + 64, pe)) to lanes (lane
+// l takes group pb + l) and issues their loads; pb is a chunk boundary.  An
+// idle pass (pb >= pe) has every lane inactive and pend = pb.
+__device__ __forceinline__ void fetch_pass_il(PassIl& a, const Streams& st, const SegInfo* seg, int* scr,
+                                              uint32_t pb, int icur, int i_end, uint32_t pe, int lane) {
+  a.live = false;
+  a.xs = 0.f;
+  a.hl = a.el = 0;
+  a.first = true;
+  a.pend = pb;
+  a.next_seg = icur;
+  a.cont = false;
+  uint32_t gl = 0u;
+  if (pb < pe) {   // wavefront-uniform
+    const int tag = -static_cast<int>(pb) - 1;
+    const int j = icur + 1 + lane;   // only segments icur+1 .. icur+64 can start in the pass
+    if (j < i_end) {
+      const uint32_t o = seg[j].off;
+      if (o < pb + kWave) scr[o - pb] = tag;
+    }
+    wave_lds_sync();
+    const uint32_t fl = scr[lane] == tag ? 1u : 0u;
+    const int cum = static_cast<int>(lanes_below(__ballot(fl))) + static_cast<int>(fl);
+    const int sid = min(icur + cum, i_end - 1);
+    const SegInfo si = seg[sid];
+    const uint32_t f = pb + static_cast<uint32_t>(lane);
+    const uint32_t fe = min(pb + static_cast<uint32_t>(kWave), pe);
+    const int ll = static_cast<int>(fe - 1u - pb);   // the last lane that may hold a group
+    const uint32_t s_off = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(si.off), ll));
+    const uint32_t s_end = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(si.off + si.cnt), ll));
+    const int s_id = __builtin_amdgcn_readlane(sid, ll);
+    // the last chunk boundary at or before fe
+    const uint32_t pend = s_end > fe ? s_off + ((fe - s_off) & ~static_cast<uint32_t>(kChunk - 1)) : fe;
+    a.pend = pend;
+    a.next_seg = min(pend < s_end ? s_id : s_id + 1, i_end - 1);
+    a.cont = s_end > pend;
+    const bool lv = f < pend;
+    const uint32_t h = si.off + ((f - si.off) & ~static_cast<uint32_t>(kChunk - 1));
+    const uint32_t ce = min(h + static_cast<uint32_t>(kChunk), si.off + si.cnt);
+    a.hl = static_cast<int>(h - pb);
+    a.el = static_cast<int>(ce - 1u - pb);
+    a.first = h == si.off;
+    a.xs = si.xs;
+    a.live = lv;
+    gl = lv ? si.gstart + (f - si.off) : 0u;
+  }
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(st.values, static_cast<int>(gl << 4), 0, kStreamPolicy);
+  a.v = make_uint4(v[0], v[1], v[2], v[3]);
+  a.rw = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>(gl << 2), 0, 0);
+}
+
+// Decodes one interleaved pass and adds its products.  Slot j of the lanes
+// of a chunk holds consecutive row-order entries, so the row of (lane, slot
+// j) is 4 * (sum over the chunk's slots before j of all their (run + 1))
+// + 4 * (sum of slot j's (run + 1) over the chunk's lanes up to this one)
+// - 4, from the chunk's start; a chunk that goes on from the previous pass
+// starts at carry4.  The eight slot sums are four wavefront scans of 16-bit
+// pairs (each field at most 64 * 64 = 4096), read back at the chunk's head
+// and last lane through LDS.  Returns the segment-relative end of the chunk
+// of lane last_lane (the pass's last group: the next pass's carry when its
+// segment goes on), wavefront-uniform.
+__device__ __forceinline__ int accumulate_pass_il(const PassIl& a, int carry4, int base4_cap, uint32_t tile_lds,
+                                                  int* scr, int lane, int last_lane) {
+  const uint32_t rw = a.live ? a.rw : 0u;
+  const uint32_t E = rw & 0x0F0F0F0Fu, O = (rw >> 4) & 0x0F0F0F0Fu;   // bytes: runs of slots 0,2,4,6 / 1,3,5,7
+  // pair q: slot 2q in bits 0..15, slot 2q + 1 in bits 16..31, each 4 * (run + 1)
+  const uint32_t live4 = a.live ? 0x00040004u : 0u;
+  uint32_t P[4];
+  P[0] = (__builtin_amdgcn_perm(O, E, 0x0C040C00u) << 2) + live4;
+  P[1] = (__builtin_amdgcn_perm(O, E, 0x0C050C01u) << 2) + live4;
+  P[2] = (__builtin_amdgcn_perm(O, E, 0x0C060C02u) << 2) + live4;
+  P[3] = (__builtin_amdgcn_perm(O, E, 0x0C070C03u) << 2) + live4;
+  uint4 S;
+  S.x = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(P[0])));
+  S.y = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(P[1])));
+  S.z = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(P[2])));
+  S.w = static_cast<uint32_t>(wave_inclusive_scan(static_cast<int>(P[3])));
+  uint4* scr4 = reinterpret_cast<uint4*>(scr);
+  scr4[lane] = S;
+  wave_lds_sync();
+  const uint4 Xh = a.hl > 0 ? scr4[a.hl - 1] : make_uint4(0u, 0u, 0u, 0u);   // before the chunk's head
+  const uint4 Z = scr4[a.el];                                               // through its last lane
+  // no field borrows: the scans are non-decreasing in every field
+  const uint32_t I0 = S.x - Xh.x, I1 = S.y - Xh.y, I2 = S.z - Xh.z, I3 = S.w - Xh.w;
+  const uint32_t T0 = Z.x - Xh.x, T1 = Z.y - Xh.y, T2 = Z.z - Xh.z, T3 = Z.w - Xh.w;
+  // slot bases: the chunk's totals of the slots before each
+  const uint32_t b1 = T0 & 0xFFFFu, b2 = b1 + (T0 >> 16), b3 = b2 + (T1 & 0xFFFFu), b4 = b3 + (T1 >> 16);
+  const uint32_t b5 = b4 + (T2 & 0xFFFFu), b6 = b5 + (T2 >> 16), b7 = b6 + (T3 & 0xFFFFu), span = b7 + (T3 >> 16);
+  // base + index sums per pair (fields below 8 * 4096 = 2^15: no carry)
+  const uint32_t Q0 = I0 + (b1 << 16), Q1 = I1 + (b2 | (b3 << 16)), Q2 = I2 + (b4 | (b5 << 16));
+  const uint32_t Q3 = I3 + (b6 | (b7 << 16));
+  const int cb4 = a.first ? 0 : carry4;
+  if (a.live) {
+    const float xs = a.xs;
+    // entry address: the chunk's start - 4 + its field, capped to the tile's
+    // slack (a corrupt stream stays inside the tile)
+    const uint32_t base = static_cast<uint32_t>(cb4 - 4) + tile_lds;
+    const uint32_t cap = static_cast<uint32_t>(base4_cap) + tile_lds;
+    tile_add_at(min(add_word<0>(base, Q0), cap), round_to_fixed(mul_lo_f16(a.v.x, xs)));
+    tile_add_at(min(add_word<1>(base, Q0), cap), round_to_fixed(mul_hi_f16(a.v.x, xs)));
+    tile_add_at(min(add_word<0>(base, Q1), cap), round_to_fixed(mul_lo_f16(a.v.y, xs)));
+    tile_add_at(min(add_word<1>(base, Q1), cap), round_to_fixed(mul_hi_f16(a.v.y, xs)));
+    tile_add_at(min(add_word<0>(base, Q2), cap), round_to_fixed(mul_lo_f16(a.v.z, xs)));
+    tile_add_at(min(add_word<1>(base, Q2), cap), round_to_fixed(mul_hi_f16(a.v.z, xs)));
+    tile_add_at(min(add_word<0>(base, Q3), cap), round_to_fixed(mul_lo_f16(a.v.w, xs)));
+    tile_add_at(min(add_word<1>(base, Q3), cap), round_to_fixed(mul_hi_f16(a.v.w, xs)));
+  }
+  return __builtin_amdgcn_readlane(cb4 + static_cast<int>(span), last_lane);
 }
 
 struct KernelArgs {
@@ -474,15 +710,16 @@ struct Early {
 };
 
 // One workgroup's share of product p: row tile and column slice number blk.
-template <int WAVES, int G, int DEPTH>
+template <int WAVES, int G, int DEPTH, int VAR>
 __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p, int blk) {
+  static_assert(VAR == kVarRlc || G == 1, "the other variants take one group per lane");
   constexpr int NT = WAVES * kWave;
   extern __shared__ __align__(16) unsigned char smem[];
   int* tile = reinterpret_cast<int*>(smem);
   // the tile's LDS byte address (for the accumulation's own LDS instructions)
   const uint32_t tile_lds = static_cast<uint32_t>(
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem));
-  const LdsLayout lay = lds_layout(e.R, e.Kc, WAVES, G);
+  const LdsLayout lay = lds_layout(e.R, e.Kc, WAVES, scr_words_of(G, VAR));
   SegInfo* seg = reinterpret_cast<SegInfo*>(smem + lay.seg_off);
   int* scr_all = reinterpret_cast<int*>(smem + lay.scr_off);
   uint32_t* part = reinterpret_cast<uint32_t*>(smem + lay.misc_off);   // 3*WAVES: the selection's scan
@@ -527,7 +764,7 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   const int base4_cap = 4 * (e.R + 7);   // tile byte address cap of a group base
 
   for (int i = tid; i < lay.tile_slots; i += NT) tile[i] = 0;
-  for (int i = tid; i < NT * G; i += NT) scr_all[i] = 0;
+  for (int i = tid; i < NT * scr_words_of(G, VAR); i += NT) scr_all[i] = 0;
   int scale = 0;   // the workgroup's fixed-point scale 2^scale
 
   // ---- selection of this slice's active, non-empty columns ----------------
@@ -592,72 +829,136 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
   // i_begin.  Segments past the range are never assigned to a live lane, so
   // the walk's segment bound is simply n_seg.
   const int wvu = __builtin_amdgcn_readfirstlane(wv);
-  const uint32_t pb0 = cut_of<WAVES>(wvu, n_grp);
-  const uint32_t pe = cut_of<WAVES>(wvu + 1, n_grp);
-  if (pb0 < pe) {
-    SegInfo s0;
-    const int i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
-    const int i_end = static_cast<int>(n_seg);
-    const Streams st = make_streams(p.values, p.runs, p.n_groups);
-    int* scr = scr_all + wv * kWave * G;
-    const int n_pass = static_cast<int>((pe - pb0 + P - 1) / P);
-    // A range that starts inside a segment starts at the row reached by the
-    // segment's earlier groups: their runs (up to 4 * 64 groups here, the
-    // rest below) are loaded ahead of the ring, so that their round trip
-    // overlaps the ring's.
-    const uint32_t before = pb0 - s0.off;
-    uint32_t rb[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (before > static_cast<uint32_t>(q * kWave)) {   // wavefront-uniform
-        // lanes past the earlier groups reread the last of them (their own
-        // lines, not one line shared by every wavefront)
-        const uint32_t j = min(static_cast<uint32_t>(q * kWave + lane), before - 1u);
-        rb[q] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + j) << 2), 0, 0);
-      }
-    }
-    Pass<G> ring[DEPTH];
-    uint32_t pf = pb0;    // flat start of the next pass to fetch
-    int icur = i_begin;   // segment holding group pf
-#pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      fetch_pass<G>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
-      icur = next_pass_segment<G>(ring[d], pf, i_end);
-      pf += P;
-    }
-    uint32_t pb = pb0;    // flat start of the pass being accumulated
-    int carry = 0;        // 4 * sum of (run + 1) over its first segment's earlier groups
-    if (before > 0u) {
-      int acc = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) acc += static_cast<uint32_t>(q * kWave + lane) < before ? group_span4(rb[q]) : 0;
-      for (uint32_t j = 4 * kWave + lane; j - lane < before; j += kWave) {   // segments longer than 256 groups
-        const uint32_t rw =
-            __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + min(j, before - 1u)) << 2), 0, 0);
-        acc += j < before ? group_span4(rw) : 0;
-      }
-      carry = __builtin_amdgcn_readlane(wave_inclusive_scan(acc), kWave - 1);
-    }
-    for (int done = 0; done < n_pass; done += DEPTH) {
+  if constexpr (VAR == kVarInterleaved) {
+    // ranges and passes cut at chunk boundaries (the same function of the
+    // equal cuts for every wavefront, so the ranges still tile the sequence)
+    const uint32_t pb0 = chunk_boundary(seg, static_cast<int>(n_seg), n_grp, cut_of<WAVES>(wvu, n_grp), lane);
+    const uint32_t pe = chunk_boundary(seg, static_cast<int>(n_seg), n_grp, cut_of<WAVES>(wvu + 1, n_grp), lane);
+    if (pb0 < pe) {
+      SegInfo s0;
+      const int i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
+      const int i_end = static_cast<int>(n_seg);
+      const Streams st = make_streams(p.values, p.runs, p.n_groups, 4u);
+      int* scr = scr_all + wv * kWave * scr_words_of(G, VAR);
+      PassIl ring[DEPTH];
+      uint32_t pf = pb0;    // flat start of the next pass to fetch
+      int icur = i_begin;   // segment holding group pf
 #pragma unroll
       for (int d = 0; d < DEPTH; ++d) {
-        if (pb < pe) {   // wavefront-uniform
-          const int tail = accumulate_pass<G>(ring[d], carry, base4_cap, tile_lds, scr, lane);
-          carry = ring[d].end63 > pb + P ? tail : 0;
+        fetch_pass_il(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
+        icur = ring[d].next_seg;
+        pf = ring[d].pend;
+      }
+      // a range that starts inside a segment starts after whole chunks of
+      // it: their span is the sum of their groups' spans, in any order (read
+      // while the ring's loads are in flight)
+      const uint32_t before = pb0 - s0.off;
+      int carry = 0;
+      if (before > 0u) {
+        int acc = 0;
+        for (uint32_t j = lane; j - lane < before; j += kWave) {
+          const uint32_t rw =
+              __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + min(j, before - 1u)) << 2), 0, 0);
+          acc += j < before ? group_span4(rw) : 0;
         }
-        pb += P;
-        fetch_pass<G>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
+        carry = __builtin_amdgcn_readlane(wave_inclusive_scan(acc), kWave - 1);
+      }
+      uint32_t pb = pb0;    // flat start of the pass being accumulated
+      // wavefront-uniform; every pass holds at least one chunk, so pe - pb0
+      // rounds of DEPTH passes are more than enough (the bound only makes
+      // termination evident)
+      for (uint32_t round = 0; pb < pe && round < pe - pb0; ++round) {
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+          if (pb < pe) {
+            const int last_lane = static_cast<int>(ring[d].pend - 1u - pb);
+            const int tail = accumulate_pass_il(ring[d], carry, base4_cap, tile_lds, scr, lane, last_lane);
+            carry = ring[d].cont ? tail : 0;
+            pb = ring[d].pend;
+          }
+          fetch_pass_il(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
+          icur = ring[d].next_seg;
+          pf = ring[d].pend;
+        }
+      }
+    }
+  } else {
+    const uint32_t pb0 = cut_of<WAVES>(wvu, n_grp);
+    const uint32_t pe = cut_of<WAVES>(wvu + 1, n_grp);
+    if (pb0 < pe) {
+      SegInfo s0;
+      const int i_begin = holding_segment(seg, static_cast<int>(n_seg), pb0, lane, s0);
+      const int i_end = static_cast<int>(n_seg);
+      const Streams st = make_streams(p.values, p.runs, p.n_groups, VAR == kVarRows16 ? 16u : 4u);
+      int* scr = scr_all + wv * kWave * scr_words_of(G, VAR);
+      const int n_pass = static_cast<int>((pe - pb0 + P - 1) / P);
+      // A range that starts inside a segment starts at the row reached by the
+      // segment's earlier groups: their runs (up to 4 * 64 groups here, the
+      // rest below) are loaded ahead of the ring, so that their round trip
+      // overlaps the ring's.
+      const uint32_t before = VAR == kVarRows16 ? 0u : pb0 - s0.off;   // row offsets need no start row
+      uint32_t rb[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (before > static_cast<uint32_t>(q * kWave)) {   // wavefront-uniform
+          // lanes past the earlier groups reread the last of them (their own
+          // lines, not one line shared by every wavefront)
+          const uint32_t j = min(static_cast<uint32_t>(q * kWave + lane), before - 1u);
+          rb[q] = __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + j) << 2), 0, 0);
+        }
+      }
+      Pass<G> ring[DEPTH];
+      const uint32_t cap_rows2 = static_cast<uint32_t>(e.R + 7) * 0x00010001u;   // both halves: R + 7
+      uint32_t pf = pb0;    // flat start of the next pass to fetch
+      int icur = i_begin;   // segment holding group pf
+#pragma unroll
+      for (int d = 0; d < DEPTH; ++d) {
+        fetch_pass<G, VAR == kVarRows16>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
         icur = next_pass_segment<G>(ring[d], pf, i_end);
         pf += P;
+      }
+      uint32_t pb = pb0;    // flat start of the pass being accumulated
+      int carry = 0;        // 4 * sum of (run + 1) over its first segment's earlier groups
+      if (before > 0u) {
+        int acc = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc += static_cast<uint32_t>(q * kWave + lane) < before ? group_span4(rb[q]) : 0;
+        for (uint32_t j = 4 * kWave + lane; j - lane < before; j += kWave) {   // segments longer than 256 groups
+          const uint32_t rw =
+              __builtin_amdgcn_raw_buffer_load_b32(st.runs, static_cast<int>((s0.gstart + min(j, before - 1u)) << 2), 0, 0);
+          acc += j < before ? group_span4(rw) : 0;
+        }
+        carry = __builtin_amdgcn_readlane(wave_inclusive_scan(acc), kWave - 1);
+      }
+      for (int done = 0; done < n_pass; done += DEPTH) {
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+          if (pb < pe) {   // wavefront-uniform
+            if constexpr (VAR == kVarRows16) {
+              accumulate_pass_rows16<G>(ring[d], cap_rows2, tile_lds);
+            } else {
+              const int tail = accumulate_pass<G, VAR == kVarSwizzle>(ring[d], carry, base4_cap, tile_lds, scr, lane);
+              carry = ring[d].end63 > pb + P ? tail : 0;
+            }
+          }
+          pb += P;
+          fetch_pass<G, VAR == kVarRows16>(ring[d], st, seg, scr, pf, icur, i_end, pe, lane);
+          icur = next_pass_segment<G>(ring[d], pf, i_end);
+          pf += P;
+        }
       }
     }
   }
   __syncthreads();
 
   // ---- merge --------------------------------------------------------------
+  // the tile slot of row r
+  const auto slot = [](int r) -> int {
+    return VAR == kVarSwizzle ? static_cast<int>(swizzle4(4u * static_cast<uint32_t>(r)) >> 2) : r;
+  };
   if (e.KC == 1) {
     for (int r = tid; r < rows; r += NT)
-      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[r]), -scale));
+      p.y[row0 + r] = float_to_half_bits(ldexpf(static_cast<float>(tile[slot(r)]), -scale));
     return;
   }
   // Row r of the product owns two 64-bit words of the workspace: ws[r]
@@ -723,7 +1024,7 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         const int r = r0 + j * NT;
-        const int q = r < rows ? tile[r] : 0;
+        const int q = r < rows ? tile[slot(r)] : 0;
         if ((q < 0 ? -q : q) <= lim) {
           ticket[j] = fine_ticket(q);
         } else {   // rare: the excess first, ordered before every ticket below
@@ -751,21 +1052,22 @@ __device__ __forceinline__ void spmspv_block(const Early& e, const KernelArgs& p
     merge_rows(std::integral_constant<int, 4>{});
 }
 
-template <int WAVES, int G, int DEPTH>
+template <int WAVES, int G, int DEPTH, int VAR>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_kernel(const uint32_t* gptr, const unsigned short* x,
                                                                 const unsigned short* colmax, int K, int Kc, int KC,
                                                                 float tau, int R, int M, KernelArgs p) {
-  spmspv_block<WAVES, G, DEPTH>(Early{gptr, x, colmax, K, Kc, KC, tau, R, M}, p,
-                                static_cast<int>(blockIdx.x));
+  spmspv_block<WAVES, G, DEPTH, VAR>(Early{gptr, x, colmax, K, Kc, KC, tau, R, M}, p,
+                                     static_cast<int>(blockIdx.x));
 }
 
+// (several products: the RLC layout and the plain tile only)
 template <int WAVES, int G, int DEPTH>
 __global__ __launch_bounds__(WAVES * kWave) void spmspv_batch_kernel(BatchArgs ba) {
   const int pi = static_cast<int>(blockIdx.y);
   if (static_cast<int>(blockIdx.x) >= ba.blocks[pi]) return;   // past this product's grid
   const KernelArgs& p = ba.prod[pi];
-  spmspv_block<WAVES, G, DEPTH>(Early{p.gptr, p.x, p.colmax, p.K, p.Kc, p.KC, p.tau, p.R, p.M},
-                                p, static_cast<int>(blockIdx.x));
+  spmspv_block<WAVES, G, DEPTH, kVarRlc>(Early{p.gptr, p.x, p.colmax, p.K, p.Kc, p.KC, p.tau, p.R, p.M},
+                                         p, static_cast<int>(blockIdx.x));
 }
 
 // Zero-fills n bytes at p: the bytes before the first 8-byte boundary, then
@@ -788,7 +1090,7 @@ __global__ __launch_bounds__(256) void zero_fill_kernel(unsigned char* p, size_t
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Plan {
-  int waves = 4, groups = 1, Kc = 0, KC = 0, T = 0;
+  int waves = 4, groups = 1, Kc = 0, KC = 0, T = 0, var = kVarRlc;
   int64_t blocks = 0;
   size_t lds = 0;
 };
@@ -796,7 +1098,10 @@ struct Plan {
 celty_status check_header(const celty_rlc_csc* W) {
   if (!W) return CELTY_EINVAL;
   if (W->version != CELTY_FORMAT_VERSION || W->run_bits != CELTY_RUN_BITS) return CELTY_EINVAL;
-  if (W->layout != CELTY_LAYOUT_RLC) return CELTY_EINVAL;
+  if (W->layout != CELTY_LAYOUT_RLC && W->layout != CELTY_LAYOUT_ROWS16 && W->layout != CELTY_LAYOUT_INTERLEAVED)
+    return CELTY_EINVAL;
+  // 16-bit row offsets: four times R + 7 fits in 16 bits
+  if (W->layout == CELTY_LAYOUT_ROWS16 && W->R > 16376) return CELTY_EINVAL;
   if (W->M < 1 || W->K < 1 || W->R < 1) return CELTY_EINVAL;
   if (W->T != static_cast<int32_t>((static_cast<int64_t>(W->M) + W->R - 1) / W->R)) return CELTY_EINVAL;
   if (W->n_groups < 0 || W->n_groups > static_cast<int64_t>(UINT32_MAX)) return CELTY_EINVAL;
@@ -805,7 +1110,7 @@ celty_status check_header(const celty_rlc_csc* W) {
   if (W->n_groups * 16 > static_cast<int64_t>(INT32_MAX)) return CELTY_EINVAL;
   if (W->n_groups > 0 && (!W->values || !W->runs)) return CELTY_EINVAL;
   if (!(W->max_abs >= 0.f) || std::isinf(W->max_abs)) return CELTY_EINVAL;
-  if (misaligned(W->values, 16) || misaligned(W->runs, 4)) return CELTY_EINVAL;
+  if (misaligned(W->values, 16) || misaligned(W->runs, W->layout == CELTY_LAYOUT_ROWS16 ? 16 : 4)) return CELTY_EINVAL;
   if (!W->colmax || misaligned(W->colmax, 4)) return CELTY_EINVAL;
   return CELTY_OK;
 }
@@ -852,8 +1157,19 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
   // bank conflicts than the bookkeeping it saves
   pl.groups = (cfg && cfg->groups_per_lane) ? cfg->groups_per_lane : 1;
   if (pl.groups != 1 && pl.groups != 2 && pl.groups != 4) return CELTY_EINVAL;
+  // the variant: the layout's row encoding, or the swizzled tile (RLC only);
+  // all but the plain RLC kernel take one group per lane
+  const int swz = cfg ? cfg->lds_swizzle : 0;
+  if (swz != 0 && swz != 1) return CELTY_EINVAL;
+  if (W->layout == CELTY_LAYOUT_RLC)
+    pl.var = swz ? kVarSwizzle : kVarRlc;
+  else if (swz)
+    return CELTY_EINVAL;
+  else
+    pl.var = W->layout == CELTY_LAYOUT_ROWS16 ? kVarRows16 : kVarInterleaved;
+  if (pl.var != kVarRlc && pl.groups != 1) return CELTY_EINVAL;
   if (W->R > kMaxLds / 4) return CELTY_EINVAL;   // keeps the layout arithmetic in int
-  pl.lds = static_cast<size_t>(lds_layout(W->R, pl.Kc, pl.waves, pl.groups).bytes);
+  pl.lds = static_cast<size_t>(lds_layout(W->R, pl.Kc, pl.waves, scr_words_of(pl.groups, pl.var)).bytes);
   if (pl.lds > static_cast<size_t>(kMaxLds)) return CELTY_EINVAL;
   pl.blocks = static_cast<int64_t>(W->T) * pl.KC;
   if (pl.blocks > 0x7FFFFFFF) return CELTY_EINVAL;
@@ -862,7 +1178,7 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
 
 // The launch: products, the largest per-product grid and LDS footprint.
 struct Launch {
-  int waves = 8, groups = 1, n = 0;
+  int waves = 8, groups = 1, n = 0, var = kVarRlc;
   bool shallow = false;   // one group per lane with a ring of two passes instead of three
   int64_t max_blocks = 0;
   size_t lds = 0;
@@ -884,31 +1200,48 @@ bool allow_large_lds(F* fn, std::atomic<uint64_t>& done) {
   return true;
 }
 
-template <int WAVES, int G, int DEPTH>
+template <int WAVES, int G, int DEPTH, int VAR>
 celty_status launch_shape(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
   static std::atomic<uint64_t> single_attr{0}, batch_attr{0};
   if (ln.n == 1) {
-    if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_kernel<WAVES, G, DEPTH>, single_attr)) return CELTY_EHIP;
+    if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_kernel<WAVES, G, DEPTH, VAR>, single_attr))
+      return CELTY_EHIP;
     const KernelArgs& q = a.prod[0];
-    hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH>), dim3(static_cast<unsigned>(ln.max_blocks)),
+    hipLaunchKernelGGL((spmspv_kernel<WAVES, G, DEPTH, VAR>), dim3(static_cast<unsigned>(ln.max_blocks)),
                        dim3(WAVES * kWave), ln.lds, stream, q.gptr, q.x, q.colmax, q.K, q.Kc, q.KC, q.tau, q.R,
                        q.M, q);
-  } else {
+  } else if constexpr (VAR == kVarRlc) {
     if (ln.lds > 64 * 1024 && !allow_large_lds(&spmspv_batch_kernel<WAVES, G, DEPTH>, batch_attr))
       return CELTY_EHIP;
     hipLaunchKernelGGL((spmspv_batch_kernel<WAVES, G, DEPTH>),
                        dim3(static_cast<unsigned>(ln.max_blocks), static_cast<unsigned>(ln.n)),
                        dim3(WAVES * kWave), ln.lds, stream, a);
+  } else {
+    return CELTY_EINVAL;   // rejected by celty_spmspv_batch before this point
   }
   return hipGetLastError() == hipSuccess ? CELTY_OK : CELTY_EHIP;
 }
 
+template <int WAVES, int VAR>
+celty_status launch_depth(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
+  return ln.shallow ? launch_shape<WAVES, 1, 2, VAR>(ln, a, stream) : launch_shape<WAVES, 1, 3, VAR>(ln, a, stream);
+}
+
 template <int WAVES>
 celty_status launch_groups(const Launch& ln, const BatchArgs& a, hipStream_t stream) {
+  if (ln.var != kVarRlc) {
+    if (ln.groups != 1 || ln.n != 1) return CELTY_EINVAL;
+    switch (ln.var) {
+      case kVarSwizzle: return launch_depth<WAVES, kVarSwizzle>(ln, a, stream);
+      case kVarRows16: return launch_depth<WAVES, kVarRows16>(ln, a, stream);
+      case kVarInterleaved: return launch_depth<WAVES, kVarInterleaved>(ln, a, stream);
+      default: return CELTY_EINVAL;
+    }
+  }
   switch (ln.groups) {
-    case 1: return ln.shallow ? launch_shape<WAVES, 1, 2>(ln, a, stream) : launch_shape<WAVES, 1, 3>(ln, a, stream);
-    case 2: return launch_shape<WAVES, 2, 2>(ln, a, stream);
-    case 4: return launch_shape<WAVES, 4, 2>(ln, a, stream);
+    case 1: return launch_depth<WAVES, kVarRlc>(ln, a, stream);
+    case 2: return launch_shape<WAVES, 2, 2, kVarRlc>(ln, a, stream);
+    case 4: return launch_shape<WAVES, 4, 2, kVarRlc>(ln, a, stream);
     default: return CELTY_EINVAL;
   }
 }
@@ -1029,6 +1362,7 @@ extern "C" celty_status celty_spmspv_plan(const celty_rlc_csc* W, const celty_la
   resolved->cols_per_block = pl.Kc;
   resolved->waves_per_block = pl.waves;
   resolved->groups_per_lane = pl.groups;
+  resolved->lds_swizzle = pl.var == kVarSwizzle ? 1 : 0;
   if (n_blocks) *n_blocks = pl.blocks;
   if (lds_bytes) *lds_bytes = static_cast<int64_t>(pl.lds);
   return CELTY_OK;
@@ -1066,7 +1400,8 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
       if (W[i]->R >= 1024) ln.waves = 16;
   }
   ln.groups = (launch_cfg && launch_cfg->groups_per_lane) ? launch_cfg->groups_per_lane : 1;
-  const celty_launch cfg{launch_cfg ? launch_cfg->cols_per_block : 0, ln.waves, ln.groups};
+  const celty_launch cfg{launch_cfg ? launch_cfg->cols_per_block : 0, ln.waves, ln.groups,
+                         launch_cfg ? launch_cfg->lds_swizzle : 0};
   const size_t need = celty_spmspv_batch_workspace_bytes(n, W);
   if (!workspace || misaligned(workspace, 256) || workspace_bytes < need) return CELTY_EINVAL;
 
@@ -1078,6 +1413,9 @@ extern "C" celty_status celty_spmspv_batch(int32_t n, const celty_rlc_csc* const
   for (int i = 0; i < n; ++i) {
     Plan pl;
     if (celty_status st = make_plan(W[i], &cfg, pl)) return st;
+    // the swizzled tile and the other layouts run one product per launch
+    if (n > 1 && pl.var != kVarRlc) return CELTY_EINVAL;
+    ln.var = pl.var;
     void* ws_i = static_cast<unsigned char*>(workspace) + ws_off;
     if (celty_status st = product_args(W[i], pl, x[i], tau[i], y[i], ws_i, ba.prod[i])) return st;
     ws_off += celty_spmspv_workspace_bytes(W[i]->M, W[i]->K, W[i]->R);

@@ -107,3 +107,96 @@ def test_header_max_abs(M, K, R):
     e2 = celty.celty_encode(Ws, None, 2)
     assert e2.max_abs == float(np.abs(Ws.astype(np.float32)).max())
     assert celty.celty_encode(np.zeros((3, 3), np.float16), None, 2).max_abs == 0.0
+
+
+# ---------------------------------------------------------------------------
+# The two other layouts: bit-exact with the oracle's encoders
+# ---------------------------------------------------------------------------
+from oracle import layouts  # noqa: E402
+
+LAYOUT_SHAPES = [(1, 1, 1), (9, 1, 4), (7, 8, 3), (65, 63, 16), (200, 31, 1000), (1025, 17, 256), (300, 40, 7),
+                 (2100, 3, 2048)]
+
+
+@pytest.mark.parametrize("M,K,R", LAYOUT_SHAPES)
+@pytest.mark.parametrize("ws", [0, 60, 95])
+def test_rows16_encoder_matches_oracle(M, K, R, ws):
+    p = workloads.random_small(M * 5 + K + R + ws, M, K, ws=ws, as_=50, zero_weights=3)
+    enc = celty.celty_encode(p.W, p.mask, R, layout=celty.LAYOUT_ROWS16)
+    ref = layouts.encode_rows16(p.W, p.mask, R)
+    assert enc.layout == celty.LAYOUT_ROWS16
+    assert enc.n_groups == ref.n_groups and enc.n_nnz == ref.n_nnz == enc.n_entries and enc.n_pad == 0
+    assert np.array_equal(enc.gptr, ref.gptr)
+    assert np.array_equal(enc.values, ref.values)
+    assert np.array_equal(enc.runs.view(np.uint16), ref.rows)
+    assert np.array_equal(enc.colmax, ref.colmax)
+    assert celty.celty_encode_plan(p.W, p.mask, R, celty.LAYOUT_ROWS16) == (ref.n_groups, ref.n_nnz, 0)
+    Wd, md = celty.celty_decode(enc)
+    stored = (p.mask != 0) & ((p.W.view(np.uint16) & 0x7FFF) != 0)
+    assert np.array_equal(md, stored.astype(np.uint8))
+    assert np.array_equal(Wd.view(np.uint16), np.where(stored, p.W.view(np.uint16), 0).astype(np.uint16))
+
+
+@pytest.mark.parametrize("M,K,R", LAYOUT_SHAPES + [(1500, 4, 1024)])
+@pytest.mark.parametrize("ws", [0, 60, 95])
+def test_interleaved_encoder_matches_oracle(M, K, R, ws):
+    p = workloads.random_small(M * 3 + K + R + ws, M, K, ws=ws, as_=50, zero_weights=3)
+    enc = celty.celty_encode(p.W, p.mask, R, layout=celty.LAYOUT_INTERLEAVED)
+    assert enc.layout == celty.LAYOUT_INTERLEAVED
+    _assert_same(enc, layouts.encode_interleaved(p.W, p.mask, R))
+    Wd, md = celty.celty_decode(enc)
+    stored = (p.mask != 0) & ((p.W.view(np.uint16) & 0x7FFF) != 0)
+    assert np.array_equal(md, stored.astype(np.uint8))
+    assert np.array_equal(Wd.view(np.uint16), np.where(stored, p.W.view(np.uint16), 0).astype(np.uint16))
+
+
+@pytest.mark.parametrize("layout", ["rows16", "interleaved"])
+@pytest.mark.parametrize("n_threads", [1, 3, 0])
+def test_layout_encoders_thread_count_does_not_matter(layout, n_threads):
+    p = workloads.random_small(9, 1500, 1100, ws=70, as_=50)
+    lay = celty.LAYOUT_ROWS16 if layout == "rows16" else celty.LAYOUT_INTERLEAVED
+    a = celty.celty_encode(p.W, p.mask, 128, n_threads=n_threads, layout=lay)
+    b = celty.celty_encode(p.W, p.mask, 128, n_threads=1, layout=lay)
+    assert np.array_equal(a.gptr, b.gptr) and np.array_equal(a.values, b.values)
+    assert np.array_equal(a.runs, b.runs)
+
+
+def test_rows16_rejects_tall_tiles():
+    W = np.ones((4, 2), dtype=np.float16)
+    with pytest.raises(celty.CeltyError):
+        celty.celty_encode_plan(W, None, 16377, celty.LAYOUT_ROWS16)
+    with pytest.raises(celty.CeltyError):
+        celty.celty_encode_plan(W, None, 4, 3)
+
+
+def test_layout_decoders_reject_corrupt_streams():
+    p = workloads.random_small(11, 120, 30, ws=50, as_=50)
+    enc = celty.celty_encode(p.W, p.mask, 64, layout=celty.LAYOUT_ROWS16)
+    rows = enc.runs.view(np.uint16)
+    seg = int(np.flatnonzero(np.diff(enc.gptr.astype(np.int64)) > 0)[0])
+    e0 = 8 * int(enc.gptr[seg])
+    # stored rows out of order
+    bad = celty.HostRlcCsc(enc.desc(), enc.gptr, enc.values, enc.runs.copy(), enc.colmax)
+    br = bad.runs.view(np.uint16)
+    if enc.values[e0 + 1] & 0x7FFF:
+        br[e0], br[e0 + 1] = rows[e0 + 1], rows[e0]
+        with pytest.raises(celty.CeltyError):
+            celty.celty_decode(bad)
+    # a stored row beyond the tile
+    bad = celty.HostRlcCsc(enc.desc(), enc.gptr, enc.values, enc.runs.copy(), enc.colmax)
+    bad.runs.view(np.uint16)[e0] = 64
+    with pytest.raises(celty.CeltyError):
+        celty.celty_decode(bad)
+    # an alignment entry at another row than the last stored one
+    n = int(np.count_nonzero(enc.values[e0:8 * int(enc.gptr[seg + 1])] & 0x7FFF))
+    if n % 8:
+        bad = celty.HostRlcCsc(enc.desc(), enc.gptr, enc.values, enc.runs.copy(), enc.colmax)
+        bad.runs.view(np.uint16)[e0 + n] ^= 1
+        with pytest.raises(celty.CeltyError):
+            celty.celty_decode(bad)
+    # an interleaved stream with a stored value moved past its segment's rows
+    il = celty.celty_encode(p.W, p.mask, 64, layout=celty.LAYOUT_INTERLEAVED)
+    bad = celty.HostRlcCsc(il.desc(), il.gptr, il.values, il.runs.copy(), il.colmax)
+    bad.runs[int(il.gptr[seg])] |= np.uint32(0xF)
+    with pytest.raises(celty.CeltyError):
+        celty.celty_decode(bad)
