@@ -567,6 +567,68 @@ def cold_dense(torch, F, p, steps: int, hot: bool = False, flush=None) -> dict:
             "timing": dense_mode}
 
 
+VARIANT_SHAPES = ((4096, 4096, 70, 70), (4096, 4096, 30, 30), (5120, 5120, 60, 60), (13824, 5120, 60, 60),
+                  (8192, 8192, 50, 60), (28672, 8192, 50, 40), (28672, 8192, 50, 60))
+
+
+def variant_study(args) -> int:
+    """The kernel's variants on the same products, in one process: the
+    paper's 4-bit runs with the plain tile (the default), the same with the
+    XOR-swizzled tile, 16-bit row offsets (no reconstruction) and the runs in
+    lane-interleaved order.  Per shape: the three encodings on rotated cold
+    copies, the four y checked bit-equal, then three rounds (alternating
+    order) of graph timing with a cache overwrite before every replay; one
+    JSON line per shape with the median µs of each variant."""
+    import torch
+
+    import paper_2608_01536_amd as celty
+    import workloads
+
+    dev = torch.device("cuda:0")
+    flush = CacheFlush(torch)
+    names = ("rlc", "swizzle", "rows16", "interleaved")
+    for (M, K, ws, as_) in VARIANT_SHAPES:
+        R = celty.default_tile_rows(M, K)
+        p = workloads.make_problem(2, M, K, ws, as_, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
+        encs = {"rlc": celty.celty_encode(p.W, p.mask, R),
+                "rows16": celty.celty_encode(p.W, p.mask, R, layout=celty.LAYOUT_ROWS16),
+                "interleaved": celty.celty_encode(p.W, p.mask, R, layout=celty.LAYOUT_INTERLEAVED)}
+        copies = {}
+        for k, e in encs.items():
+            base = e.to_device(dev)
+            copies[k] = [base] + [base.clone_to() for _ in range(max(2, -(-COLD_BYTES // stored_bytes(e))) - 1)]
+        copies["swizzle"] = copies["rlc"]
+        launch = {v: (0, 0, 0, 1 if v == "swizzle" else 0) for v in names}
+        x = torch.from_numpy(p.x.view(np.int16)).to(dev)
+        y = torch.empty(M, dtype=torch.int16, device=dev)
+        wsb = celty.new_workspace(copies["rlc"][0], dev)
+        ys = []
+        for v in names:
+            celty.celty_spmspv_ex(copies[v][0], x, p.tau, y, wsb, launch[v])
+            torch.cuda.synchronize()
+            ys.append(y.cpu().numpy().copy())
+        same = all(np.array_equal(ys[0], o) for o in ys[1:])
+        res = {v: [] for v in names}
+        for rnd in range(3):
+            for v in (names if rnd % 2 == 0 else names[::-1]):
+                cs = copies[v]
+                us, _ = time_graph(torch, lambda i, cs=cs, v=v: celty.celty_spmspv_ex(cs[i % len(cs)], x, p.tau, y, wsb,
+                                                                                     launch[v]),
+                                   args.steps, replays=3, flush=flush)
+                res[v].append(us)
+        b_alg = algorithmic_bytes_from_encoding(encs["rlc"], p.x, p.tau)[0]
+        med = {v: round(float(np.median(res[v])), 3) for v in names}
+        print(json.dumps({"study": "kernel variants", "shape": f"{M}x{K}", "ws": ws, "as": as_, "R": R,
+                          "us": med, "y_bit_equal": same, "algorithmic_bytes": b_alg,
+                          "stored_bytes": {k: stored_bytes(e) for k, e in encs.items()}, "steps": args.steps}),
+              flush=True)
+        del copies, encs
+        torch.cuda.empty_cache()
+        if not same:
+            return 1
+    return 0
+
+
 PAPER_SHAPES = ((4096, 4096), (4096, 11008), (5120, 5120), (5120, 13824), (7168, 7168), (7168, 28672))
 
 
@@ -683,6 +745,9 @@ def main() -> int:
     ap.add_argument("--no-fused", action="store_true", help="--sequence without the stacked-encoding schedule")
     ap.add_argument("--format-study", action="store_true",
                     help="host only: RLC-CSC vs bitmap vs dense sizes across weight sparsity")
+    ap.add_argument("--variant-study", action="store_true",
+                    help="the kernel variants (swizzled tile, 16-bit rows, interleaved runs) against the default, "
+                         "one process, seven shapes")
     ap.add_argument("--paper-shapes", action="store_true",
                     help="the paper's six kernel shapes at 30/50/70%% dual sparsity vs dense GEMV")
     ap.add_argument("--encode-throughput", action="store_true",
@@ -704,6 +769,8 @@ def main() -> int:
         return sequence_bench(args)
     if args.paper_shapes:
         return paper_shapes(args)
+    if args.variant_study:
+        return variant_study(args)
 
     import torch
     import torch.nn.functional as F
