@@ -263,6 +263,7 @@ def sequence_bench(args) -> int:
     xs = [None] * n_layers              # per layer: device x of each projection
     taus = [None] * n_layers
     alg_step = 0.0
+    algs = [None] * n_layers            # per layer: algorithmic bytes of the 7 projections
     stored_step = 0
     dense_shapes = None
     done = 0
@@ -275,6 +276,7 @@ def sequence_bench(args) -> int:
         xd = {k: torch.from_numpy(v.view(np.int16)).to(dev) for k, v in xh.items()}
         xs[layer] = [xd[pr.x_group] for pr in c["layers"]]
         taus[layer] = tl
+        algs[layer] = alg
         alg_step += sum(alg)
         stored_step += sum(stored_bytes(e) for e in encs)
         del encs, stacked
@@ -345,6 +347,32 @@ def sequence_bench(args) -> int:
         out["dense_note"] = ("sum over the layer's shapes of F.linear fp16 batch-1 times (cold copies, caches "
                              "overwritten before each timed replay) x layers")
         out["speedup_vs_dense"] = {k: round(d_step / out[k]["us_per_step"], 3) for k, _, _ in schedules}
+    if fused_on and not args.no_read_floor:
+        # the fused schedule's launches as plain reads of their algorithmic
+        # bytes (one launch per x-group and layer, in order, distinct bytes)
+        del layers, fused
+        torch.cuda.empty_cache()
+        sizes = [[max(16, int(sum(algs[l][i] for i in g)) // 16 * 16) for g in groups] for l in range(n_layers)]
+        buf = torch.empty(sum(sum(s) for s in sizes), dtype=torch.uint8, device=dev)
+        buf.fill_(1)
+        sink = torch.empty(1024, dtype=torch.int32, device=dev)
+
+        def step_read(s):
+            off = 0
+            for l in range(n_layers):
+                for nb in sizes[l]:
+                    celty.celty_bench_stream_read(buf[off:off + nb], nb, sink, 512, 512)
+                    off += nb
+
+        step_read(0)
+        torch.cuda.synchronize()
+        us, _ = time_graph(torch, step_read, reps, replays=3, flush=flush)
+        out["read_floor"] = {"us_per_step": round(us, 2), "GBps": round(alg_step / us / 1e3, 1),
+                             "pct_peak_hbm": round(100 * alg_step / us / 1e3 / PEAK_HBM_GBPS, 2),
+                             "fused_vs_floor": round(us / out["fused"]["us_per_step"], 3),
+                             "op": "the fused schedule's launches as plain streaming reads of their algorithmic "
+                                   "bytes (celty_bench_stream_read, 512 x 512 lanes)"}
+        print(f"[sequence] read floor: {us:.1f} us/step", file=sys.stderr, flush=True)
     print(json.dumps(out))
     return 0
 
@@ -543,6 +571,33 @@ def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool
     return out
 
 
+READ_SHAPES = ((256, 1024), (512, 512), (1024, 256))
+
+
+def read_floor(torch, celty, nbytes: float, steps: int, flush=None) -> dict:
+    """What the memory system gives one launch that reads nbytes: the
+    library's measurement reference (celty_bench_stream_read, a plain
+    streaming read) graph-timed on rotated cold buffers under the same
+    protocol as the product, best of three launch shapes."""
+    nb = max(16, int(nbytes) // 16 * 16)
+    nc = max(2, -(-COLD_BYTES // nb))
+    bufs = [torch.empty(nb, dtype=torch.uint8, device="cuda") for _ in range(nc)]
+    for b in bufs:
+        b.fill_(1)
+    sink = torch.empty(1024, dtype=torch.int32, device="cuda")
+    best = None
+    for blocks, threads in READ_SHAPES:
+        us, _ = time_graph(torch, lambda i: celty.celty_bench_stream_read(bufs[i % nc], nb, sink, blocks, threads),
+                           steps, replays=3, flush=flush)
+        if best is None or us < best[0]:
+            best = (us, blocks, threads)
+    del bufs
+    torch.cuda.empty_cache()
+    return {"us": round(best[0], 3), "bytes": nb, "GBps": round(nb / best[0] / 1e3, 1),
+            "launch": f"{best[1]} workgroups x {best[2]} lanes",
+            "op": "celty_bench_stream_read: one launch streaming the same number of bytes, 16-byte loads"}
+
+
 def cold_dense(torch, F, p, steps: int, hot: bool = False, flush=None) -> dict:
     """The dense reference: F.linear fp16 at batch 1 on the masked W and the
     thresholded x, same cold rotation, cache overwrite and graph timing."""
@@ -722,6 +777,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-read-floor", action="store_true",
+                    help="skip the plain-read reference of the same bytes (celty_bench_stream_read)")
     ap.add_argument("--sigma", type=float, default=0.0,
                     help="outlier input features: per-feature scales exp(sigma*N(0,1)) on W's columns and x, "
                          "per-row magnitude pruning (0 = the uniform-mask workload)")
@@ -837,6 +894,7 @@ def main() -> int:
     floor_kernel, _ = time_graph(torch, lambda i: tiny.fill_(1.0), args.steps)
 
     dense = None if args.no_dense else cold_dense(torch, F, p, args.steps, args.hot, flush=flush)
+    floor_read = None if (args.hot or args.no_read_floor) else read_floor(torch, celty, b_alg, args.steps, flush)
 
     cpu = None
     if not args.no_cpu:
@@ -896,6 +954,10 @@ def main() -> int:
         "eager_us_per_call": round(eager_us, 3),
         "launch_floor": {"graph_us": round(floor_kernel, 3), "eager_us": round(floor_wall, 3),
                          "op": "one-element torch fill kernel"},
+        "read_floor": None if floor_read is None else dict(
+            floor_read, kernel_vs_floor=round(floor_read["us"] / us_step, 3),
+            note="a plain read of the algorithmic bytes in one launch; kernel_vs_floor > 1: the SpMSpV call "
+                 "takes less time than that read"),
         "dense_gemv": dense,
         "speedup_vs_dense": round(dense["us"] / us_step, 3) if dense else None,
         "cpu_baseline": cpu,

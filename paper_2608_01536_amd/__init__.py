@@ -78,6 +78,7 @@ _decode = _sig("celty_decode", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, 
 _select = _sig("celty_select", ctypes.c_int, _p, _i32, _f32, _p, _p, _p)
 _ws_bytes = _sig("celty_spmspv_workspace_bytes", _sz, _i32, _i32, _i32)
 _ws_init = _sig("celty_spmspv_workspace_init", ctypes.c_int, _p, _sz, _p)
+_stream_read = _sig("celty_bench_stream_read", ctypes.c_int, _p, _sz, _p, _i32, _i32, _p)
 _spmspv = _sig("celty_spmspv", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz, _p)
 _spmspv_ex = _sig("celty_spmspv_ex", ctypes.c_int, ctypes.POINTER(celty_rlc_csc), _p, _f32, _p, _p, _sz,
                   ctypes.POINTER(celty_launch), _p)
@@ -372,6 +373,16 @@ def celty_spmspv_plan(W, launch=None) -> dict:
                 lds_bytes=lds.value)
 
 
+def celty_bench_stream_read(buf, nbytes: int, sink, blocks: int, threads: int, stream=None) -> None:
+    """Measurement reference (include/celty_bench.h): one launch that streams
+    nbytes of the device tensor buf; sink holds at least `blocks` int32."""
+    if int(nbytes) > buf.numel() * buf.element_size():
+        raise ValueError("nbytes exceeds the buffer")
+    _check(_stream_read(_dev_ptr(buf, buf.element_size(), "buf"), int(nbytes),
+                        _dev_ptr(sink, 4, "sink", int(blocks), buf.device), int(blocks), int(threads),
+                        _stream_handle(stream)), "celty_bench_stream_read")
+
+
 def default_tile_rows(M: int, K: int) -> int:
     """Tile height R for encoding an M x K matrix (celty_default_tile_rows)."""
     return int(_default_tile_rows(int(M), int(K)))
@@ -382,5 +393,6 @@ __all__ = [
     "celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv", "celty_spmspv_ex",
     "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "new_batch_workspace", "celty_spmspv_noalloc",
     "celty_spmspv_plan", "celty_spmspv_workspace_bytes", "celty_spmspv_workspace_init", "celty_status_string",
+    "celty_bench_stream_read",
     "new_workspace", "HostRlcCsc", "DeviceRlcCsc", "CeltyError", "celty_rlc_csc", "celty_launch",
 ]

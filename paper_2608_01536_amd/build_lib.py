@@ -12,7 +12,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libcelty.so")
 SOURCES = [os.path.join(PKG, "csrc", "spmspv.hip"), os.path.join(PKG, "csrc", "select.hip"),
-           os.path.join(PKG, "csrc", "encode.cpp")]
+           os.path.join(PKG, "csrc", "encode.cpp"),
+           # a measurement reference for the benchmark (include/celty_bench.h)
+           os.path.join(PKG, "csrc", "bench_read.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

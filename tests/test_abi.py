@@ -6,6 +6,7 @@ only where no GPU is visible, so a validation bug can never launch a kernel on
 garbage pointers.
 """
 import ctypes
+import glob
 import math
 import os
 import re
@@ -19,12 +20,14 @@ from paper_2608_01536_amd import (CELTY_EFORMAT, CELTY_EINVAL, CELTY_OK, celty_l
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "celty.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def _declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    names = re.findall(r"^[A-Za-z_][\w\s\*]*?\b(celty_\w+)\s*\(", text, flags=re.M)
+    names = []
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names += re.findall(r"^[A-Za-z_][\w\s\*]*?\b(celty_\w+)\s*\(", text, flags=re.M)
     return sorted(set(names))
 
 
@@ -33,7 +36,8 @@ def test_header_declares_the_boundary():
     for want in ("celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv",
                  "celty_spmspv_ex", "celty_spmspv_plan", "celty_spmspv_workspace_bytes",
                  "celty_spmspv_workspace_init", "celty_status_string", "celty_default_tile_rows",
-                 "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes"):
+                 "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "celty_spmspv_noalloc",
+                 "celty_bench_stream_read"):
         assert want in names
 
 
@@ -368,6 +372,17 @@ def test_select_rejects_bad_arguments():
     assert f(FAKE, 10, 0.5, FAKE + 66, FAKE + 128, None) == CELTY_EINVAL
     # x's byte size must fit the kernel's 32-bit buffer size
     assert f(FAKE, 2**30, 0.5, FAKE + 64, FAKE + 128, None) == CELTY_EINVAL
+
+
+def test_stream_read_rejects_bad_arguments():
+    f = celty._stream_read
+    assert f(FAKE, 4096, None, 4, 256, None) == CELTY_EINVAL          # no sink
+    assert f(FAKE, 4096, FAKE + 2, 4, 256, None) == CELTY_EINVAL      # misaligned sink
+    assert f(FAKE + 8, 4096, FAKE, 4, 256, None) == CELTY_EINVAL      # misaligned buffer
+    assert f(None, 4096, FAKE, 4, 256, None) == CELTY_EINVAL
+    assert f(FAKE, 4100, FAKE, 4, 256, None) == CELTY_EINVAL          # not a multiple of 16
+    for blocks, threads in ((0, 256), (65536, 256), (4, 32), (4, 100), (4, 2048)):
+        assert f(FAKE, 4096, FAKE, blocks, threads, None) == CELTY_EINVAL
 
 
 def test_single_hip_runtime_alongside_torch():

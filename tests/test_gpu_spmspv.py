@@ -810,3 +810,24 @@ def test_x_only_two_byte_aligned(celty, torch_dev, M, K, R):
         torch.cuda.synchronize()
         assert int(ws.count_nonzero()) == 0
         _check(y.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
+
+
+# --------------------------------------------------------------------------
+# the benchmark's read reference (celty_bench_stream_read)
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("nbytes,blocks,threads", [(0, 4, 64), (16, 1, 64), (4096 * 16 + 48, 7, 192),
+                                                   (3 << 20, 512, 512), (5 << 20, 256, 1024)])
+def test_stream_read_reads_every_byte(celty, torch_dev, nbytes, blocks, threads):
+    # each workgroup's word is the XOR of the 32-bit words it read; the XOR
+    # of all workgroups' words is the XOR of the whole buffer
+    torch, dev = torch_dev
+    _note(f"stream read {nbytes} B, {blocks} x {threads}")
+    rng = np.random.default_rng(nbytes + blocks)
+    host = rng.integers(0, 2**32, size=max(4, nbytes // 4), dtype=np.uint32)
+    buf = torch.from_numpy(host.view(np.int32)).to(dev)
+    sink = torch.full((blocks,), -1, dtype=torch.int32, device=dev)
+    celty.celty_bench_stream_read(buf, nbytes, sink, blocks, threads)
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    want = np.bitwise_xor.reduce(host[:nbytes // 4]) if nbytes else np.uint32(0)
+    assert int(got) == int(want)
