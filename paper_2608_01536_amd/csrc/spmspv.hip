@@ -1133,16 +1133,22 @@ celty_status make_plan(const celty_rlc_csc* W, const celty_launch* cfg, Plan& pl
     const int64_t n_wg = W->T * ((W->K + kc - 1) / kc);
     // Counts past the slots start a second round, and 8-wavefront counts
     // between one and 0.9 x two per compute unit leave some units with two
-    // and the rest with one: then take the most slices that fit the slots,
-    // with no rounding of the width.  Up to one workgroup per unit the count
-    // is kept (fewer, wider slices cost fewer merge tickets), and so it is
-    // when the new slices would hold under 48 KB of stored groups each,
-    // where the extra tickets (16 bytes per row and slice) outweigh the
-    // balance.
+    // and the rest with one.  Then, with no rounding of the width: slices
+    // that would hold at least 80 KB of stored groups each at two workgroups
+    // per unit take the most slices that fit the slots (two per unit);
+    // lighter ones take one workgroup per unit, whose wider slices halve the
+    // merge tickets (16 bytes per row and slice), which outweigh the second
+    // workgroup's latency hiding on light slices.  Up to one workgroup per
+    // unit the count is kept.
     const int64_t ks = std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, slots / W->T));
     const bool uneven = pl.waves == 8 && n_wg > 256 && 10 * n_wg < 9 * slots;
     const double stored_per_wg = 20.0 * static_cast<double>(W->n_groups) / static_cast<double>(W->T * ks);
-    if (n_wg > slots || (uneven && stored_per_wg >= 48.0 * 1024.0)) kc = (W->K + ks - 1) / ks;
+    if (n_wg > slots || (uneven && stored_per_wg >= 80.0 * 1024.0)) {
+      kc = (W->K + ks - 1) / ks;
+    } else if (uneven) {
+      const int64_t k1 = std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, 256 / W->T));
+      kc = (W->K + k1 - 1) / k1;
+    }
     kc = std::min<int64_t>(kc, std::min(4096, kMaxCols * kWave * pl.waves));
     Kc = static_cast<int>(kc);
   }

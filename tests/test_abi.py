@@ -201,11 +201,13 @@ def test_automatic_plan_fills_the_compute_units_in_one_even_round():
                 assert n == d.T * KC <= slots, (M, K, G, n)
                 if out.waves_per_block == 8 and 256 < n < 0.9 * slots:
                     assert out.cols_per_block % 64 == 0 or out.cols_per_block == K or KC == 63, (M, K, G, n)
-    # 5120 x 13824 at half density: 10 tiles x 51 slices; 5120 x 5120 with
-    # little stored data keeps 10 x 40
+    # 5120 x 13824 at half density: 10 tiles x 51 slices (two workgroups per
+    # unit); 5120 x 5120 with light slices (under 80 KB of stored groups at
+    # two per unit) takes one per unit, 10 x 25; with heavy slices 10 x 51
     assert plan(5120, 13824, 5120 * 13824 // 16)[2] == 510
-    assert plan(5120, 5120, 1000)[2] == 400
-    assert plan(5120, 5120, 5120 * 5120 // 16)[2] == 510
+    assert plan(5120, 5120, 1000)[2] == 250
+    assert plan(5120, 5120, 5120 * 5120 // 16)[2] == 250
+    assert plan(5120, 5120, 5120 * 5120 // 8)[2] == 510
 
 
 @host_only
