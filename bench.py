@@ -860,7 +860,7 @@ def main() -> int:
                 (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "") + \
                 variant_flags
         cmds = [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py "
-                f"--steps 200 --warmup 20 --no-cpu --no-dense{flags}" for c in ("FETCH_SIZE", "WRITE_SIZE")]
+                f"--steps 200 --warmup 20 --no-cpu --no-dense --no-read-floor{flags}" for c in ("FETCH_SIZE", "WRITE_SIZE")]
         cmds += [f"rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- python3 bench.py --copy-calibration"
                  for c in ("FETCH_SIZE", "WRITE_SIZE")]
         return record_traffic(workload_key, args.record_traffic, cmds)
@@ -870,7 +870,7 @@ def main() -> int:
                 (f" --cols {args.cols}" if args.cols else "") + (f" --waves {args.waves}" if args.waves else "") + \
                 variant_flags
         cmd = (f"rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o run -- python3 bench.py "
-               f"--no-cpu --no-dense --steps {args.steps} --warmup {args.warmup}{flags}")
+               f"--no-cpu --no-dense --no-read-floor --steps {args.steps} --warmup {args.warmup}{flags}")
         return record_kernel_trace(workload_key, args.record_kernel_trace, cmd)
     dev = torch.device("cuda:0")
     # algorithmic bytes are those of the paper's format (RLC) for every
