@@ -700,6 +700,7 @@ def paper_shapes(args) -> int:
     import paper_2608_01536_amd as celty
     import workloads
 
+    flush = CacheFlush(torch)
     speed = {}
     for pct in (30, 50, 70):
         for (M, K) in PAPER_SHAPES:
