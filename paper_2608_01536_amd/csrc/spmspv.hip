@@ -33,6 +33,14 @@
 //     so that the last slice also reads that word.  The slice that arrives
 //     last writes y[row] in fp16 and clears the words for the next call.
 //     With a single slice the tile goes straight to y.
+//
+// Variants of the same product (for the ablations of Sections 4.1-4.2; the
+// default above is the paper's format in its stored order): 16-bit row
+// offsets loaded instead of reconstructed, the runs in lane-interleaved order
+// (each pass then holds whole chunks, and the eight slot prefixes come from
+// packed wavefront scans), and an XOR-swizzled slot order of the LDS tile.
+// Each forms the same products on the same grids, so its y is the default's
+// bit for bit.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
