@@ -562,10 +562,15 @@ def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool
         step(i)
     torch.cuda.synchronize()
     eager_us = time_loop(torch, step, steps)
+    # the same eager loop through prepared calls (arguments checked once)
+    preps = [celty.PreparedSpMSpV(c, x, y, ws, launch) for c in copies]
+    eager_prepared_us = time_loop(torch, lambda i: preps[i % ncopies](p.tau), steps)
+    del preps
     # the timed region: the steps captured in one HIP graph and replayed on
     # the launch stream; one step is exactly one kernel launch
     us, samples = time_graph(torch, step, steps, flush=None if hot else flush)
-    out = {"us": us, "samples": samples, "eager_us": eager_us, "copies": ncopies}
+    out = {"us": us, "samples": samples, "eager_us": eager_us, "eager_prepared_us": eager_prepared_us,
+           "copies": ncopies}
     del copies, base
     torch.cuda.empty_cache()
     return out
@@ -953,6 +958,7 @@ def main() -> int:
                          "dispatches": ktrace["dispatches"],
                          "source": os.path.relpath(kernel_trace_file(workload_key), ROOT)}},
         "eager_us_per_call": round(eager_us, 3),
+        "eager_us_per_call_prepared": round(run["eager_prepared_us"], 3),
         "launch_floor": {"graph_us": round(floor_kernel, 3), "eager_us": round(floor_wall, 3),
                          "op": "one-element torch fill kernel"},
         "read_floor": None if floor_read is None else dict(

@@ -228,6 +228,10 @@ celty_status celty_spmspv_workspace_init(void* workspace, size_t workspace_bytes
  *              become +0); must not alias x or the workspace.
  *   workspace  device buffer of at least celty_spmspv_workspace_bytes(M,K,R)
  *              bytes, zero-filled before first use (celty_spmspv_workspace_init).
+ *              Every completed call leaves it zero; a call that did not
+ *              complete (the device reported an error after the launch)
+ *              may leave merge words behind, so zero-fill it again before
+ *              the next call, or the next y is wrong.
  * One kernel launch.  The grid is (row tile t) x (column slice c).  Every
  * workgroup selects the active columns of its slice that store entries in
  * its tile (the n columns of A_ct), walks their compressed segments, forms

@@ -318,6 +318,32 @@ def celty_spmspv_ex(W: DeviceRlcCsc, x, tau: float, y, workspace, launch=None, s
                       None if ls is None else ctypes.byref(ls), _stream_handle(stream)), "celty_spmspv_ex")
 
 
+class PreparedSpMSpV:
+    """celty_spmspv_ex with its arguments checked and marshalled once.
+
+    For eager serving loops, where the per-call tensor checks and argument
+    conversion of celty_spmspv_ex cost more host time than the launch itself:
+    the tensors (x, y, workspace) and the stream are fixed here and must stay
+    alive and in place; each call passes only tau and goes straight to the C
+    entry point (which still validates every argument before launching)."""
+
+    def __init__(self, W: DeviceRlcCsc, x, y, workspace, launch=None, stream=None):
+        dev, hd = W.gptr.device, _half_dtypes()
+        self._keep = (W, x, y, workspace)
+        self._desc = W.desc()
+        self._ls = _launch_struct(launch)
+        self._args = (ctypes.byref(self._desc), _dev_ptr(x, 2, "x", W.K, dev, hd),
+                      _dev_ptr(y, 2, "y", W.M, dev, hd), _dev_ptr(workspace, 1, "workspace", 0, dev),
+                      workspace.numel(), None if self._ls is None else ctypes.byref(self._ls),
+                      _stream_handle(stream))
+
+    def __call__(self, tau: float) -> None:
+        d, x, y, ws, n, ls, st = self._args
+        status = _spmspv_ex(d, x, tau, y, ws, n, ls, st)
+        if status != CELTY_OK:
+            raise CeltyError(status, "celty_spmspv_ex")
+
+
 def celty_spmspv_noalloc(W: DeviceRlcCsc, x, tau: float, y, launch=None, stream=None) -> None:
     """As celty_spmspv_ex with the library's static merge array (no workspace, nothing allocated)."""
     d, dev = W.desc(), W.gptr.device
@@ -393,6 +419,6 @@ __all__ = [
     "celty_encode_plan", "celty_encode", "celty_decode", "celty_select", "celty_spmspv", "celty_spmspv_ex",
     "celty_spmspv_batch", "celty_spmspv_batch_workspace_bytes", "new_batch_workspace", "celty_spmspv_noalloc",
     "celty_spmspv_plan", "celty_spmspv_workspace_bytes", "celty_spmspv_workspace_init", "celty_status_string",
-    "celty_bench_stream_read",
+    "celty_bench_stream_read", "PreparedSpMSpV",
     "new_workspace", "HostRlcCsc", "DeviceRlcCsc", "CeltyError", "celty_rlc_csc", "celty_launch",
 ]

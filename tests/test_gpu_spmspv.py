@@ -831,3 +831,25 @@ def test_stream_read_reads_every_byte(celty, torch_dev, nbytes, blocks, threads)
     got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
     want = np.bitwise_xor.reduce(host[:nbytes // 4]) if nbytes else np.uint32(0)
     assert int(got) == int(want)
+
+
+def test_prepared_call_matches_spmspv_ex(celty, torch_dev):
+    # PreparedSpMSpV checks its tensors once; each call passes only tau
+    torch, dev = torch_dev
+    p = workloads.headline_problem(0)
+    Wd = celty.celty_encode(p.W, p.mask, 512).to_device(dev)
+    xt = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    y1 = torch.empty(p.W.shape[0], dtype=torch.int16, device=dev)
+    y2 = torch.empty_like(y1)
+    ws1, ws2 = celty.new_workspace(Wd, dev), celty.new_workspace(Wd, dev)
+    prep = celty.PreparedSpMSpV(Wd, xt, y2, ws2, (128, 4, 1))
+    for tau in (p.tau, 0.5 * p.tau, -1.0):
+        celty.celty_spmspv_ex(Wd, xt, tau, y1, ws1, (128, 4, 1))
+        prep(tau)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y2)
+    assert int(ws2.count_nonzero()) == 0
+    with pytest.raises(ValueError):
+        celty.PreparedSpMSpV(Wd, xt[:-1], y2, ws2)       # short x is refused once, here
+    with pytest.raises(celty.CeltyError):
+        prep(float("nan"))                                # the C entry point still validates tau
