@@ -82,6 +82,8 @@ CASES = [
     ("waves4", 1500, 900, 50, 50, 512, 64, 4),
     ("tall_16w", 8192, 1024, 50, 60, 1024, 0, 0),
     ("r1", 37, 50, 30, 30, 1, 0, 0),
+    ("eight_cols_per_lane", 3000, 4096, 60, 50, 512, 1024, 2),
+    ("long_ranges_2w", 4096, 96, 0, 0, 2048, 96, 2),
 ]
 
 
