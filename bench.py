@@ -10,15 +10,19 @@ single kernel launch).
 Cold cache: the encoded matrix is copied to enough distinct device buffers to
 exceed 1 GiB (beyond the 256 MiB Infinity Cache and the L2s) and the steps
 rotate over them, so every step streams its weights from HBM; before every
-timed graph replay a 1 GiB buffer is overwritten (outside the timed events),
-so the first copies a replay reads are not left in a cache by the replay
-before it, whatever the step count.
+timed graph replay (outside the timed events) 1 GiB of another buffer is
+read, so the first copies a replay reads are not left in a cache by the
+replay before it, whatever the step count, and one call on a spare copy
+re-warms the code and the small buffers.
 
 Printed (one JSON line): µs per SpMSpV (value, lower is better), effective
 GB/s on algorithmic bytes, the roofline of the kernel (HIP events around a
-graph replay of the K steps on the launch stream), the dense fp16 GEMV (torch F.linear, i.e.
-hipBLASLt/rocBLAS) on the same shape under the same cold protocol, the
-floor of a near-empty kernel, and the CPU oracle timed on a bounded sample.
+graph replay of the K steps on the launch stream; the profiler's kernel
+durations and HBM traffic from the committed records), the time of a plain
+read of the same bytes in one launch (read_floor), the dense fp16 GEMV (torch
+F.linear, i.e. hipBLASLt/rocBLAS) on the same shape under the same cold
+protocol, the floor of a near-empty kernel, eager per-call times, and the CPU
+oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -232,7 +236,7 @@ def sequence_bench(args) -> int:
     the host by a pool of worker processes and uploaded to HBM, so a step
     streams all of its distinct weights from HBM.  When the step moves less
     than 1 GiB the graph runs it several times over (each time the caches are
-    overwritten before the timed replay)."""
+    cleared before the timed replay)."""
     import concurrent.futures as cf
     import multiprocessing as mp
 
@@ -345,7 +349,7 @@ def sequence_bench(args) -> int:
         d_step = n_layers * sum(dense[sh] for sh in dense_shapes)
         out["dense_gemv_us_per_step"] = round(d_step, 2)
         out["dense_note"] = ("sum over the layer's shapes of F.linear fp16 batch-1 times (cold copies, caches "
-                             "overwritten before each timed replay) x layers")
+                             "cleared before each timed replay) x layers")
         out["speedup_vs_dense"] = {k: round(d_step / out[k]["us_per_step"], 3) for k, _, _ in schedules}
     if fused_on and not args.no_read_floor:
         # the fused schedule's launches as plain reads of their algorithmic
@@ -657,7 +661,7 @@ def variant_study(args) -> int:
     XOR-swizzled tile, 16-bit row offsets (no reconstruction) and the runs in
     lane-interleaved order.  Per shape: the three encodings on rotated cold
     copies, the four y checked bit-equal, then three rounds (alternating
-    order) of graph timing with a cache overwrite before every replay; one
+    order) of graph timing with the caches cleared before every replay; one
     JSON line per shape with the median µs of each variant."""
     import torch
 
