@@ -117,8 +117,9 @@ def recorded_kernel_trace(workload_key: str):
 def record_kernel_trace(workload_key: str, trace_csv: str, command: str) -> int:
     """Turns a rocprofv3 --kernel-trace CSV of this benchmark into the record
     recorded_kernel_trace() reads: the mean and median duration of the
-    SpMSpV dispatches of the graph replays (the last 5 * steps dispatches:
-    the warm-up and eager calls come first)."""
+    SpMSpV dispatches of the timed graph replays (the last 5 * steps
+    dispatches, which also hold four of the single re-warm calls between the
+    replays; the warm-up and eager calls come first)."""
     import csv
     import statistics
     durs = []
