@@ -7,22 +7,29 @@ batch 1 -- the "70 % dual sparsity" point.  One step = one celty_spmspv call
 (selection, compressed-column walk, LDS accumulation, merge, fp16 output: a
 single kernel launch).
 
-Cold cache: the encoded matrix is copied to enough distinct device buffers to
-exceed 1 GiB (beyond the 256 MiB Infinity Cache and the L2s) and the steps
-rotate over them, so every step streams its weights from HBM; before every
-timed graph replay (outside the timed events) 1 GiB of another buffer is
-read, so the first copies a replay reads are not left in a cache by the
-replay before it, whatever the step count, and one call on a spare copy
-re-warms the code and the small buffers.
+Cold cache: the encoded matrix is copied to enough distinct device buffers
+that the steps, rotating over them, read at least 1 GiB (beyond the 256 MiB
+Infinity Cache and the L2s) between two reads of the same copy -- counted in
+the bytes a call reads, its active columns, not in the copy's size -- so
+every step streams its weights from HBM (--cold-bytes sets the 1 GiB).
+Before every timed replay of the K steps (outside the timed events) 1 GiB
+of another buffer is read, so the first copies a replay reads are not left
+in a cache by the replay before it, whatever the step count, and one call
+on a spare copy re-warms the code and the small buffers.
+
+Timing: HIP events on the launch stream around the K steps, which are
+launched back to back and all enqueued while the GPU is still busy with the
+cache-clearing reads before the start event, so neither the host nor a graph
+launch sits inside the timed region; the same K steps as one graph replay
+are reported beside it.
 
 Printed (one JSON line): µs per SpMSpV (value, lower is better), effective
-GB/s on algorithmic bytes, the roofline of the kernel (HIP events around a
-graph replay of the K steps on the launch stream; the profiler's kernel
-durations and HBM traffic from the committed records), the time of a plain
-read of the same bytes in one launch (read_floor), the dense fp16 GEMV (torch
-F.linear, i.e. hipBLASLt/rocBLAS) on the same shape under the same cold
-protocol, the floor of a near-empty kernel, eager per-call times, and the CPU
-oracle timed on a bounded sample.
+GB/s on algorithmic bytes, the roofline of the kernel (the timing above; the
+profiler's kernel durations and HBM traffic from the committed records), the
+time of a plain read of the same bytes in one launch (read_floor), the dense
+fp16 GEMV (torch F.linear, i.e. hipBLASLt/rocBLAS) on the same shape under
+the same cold protocol and timing, the floor of a near-empty kernel, eager
+per-call times, and the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -117,9 +124,13 @@ def recorded_kernel_trace(workload_key: str):
 def record_kernel_trace(workload_key: str, trace_csv: str, command: str) -> int:
     """Turns a rocprofv3 --kernel-trace CSV of this benchmark into the record
     recorded_kernel_trace() reads: the mean and median duration of the
-    SpMSpV dispatches of the timed graph replays (the last 5 * steps
+    SpMSpV dispatches of the timed (queued) replays: the last 5 * steps
     dispatches, which also hold four of the single re-warm calls between the
-    replays; the warm-up and eager calls come first)."""
+    replays; the warm-up, eager and graph-replay calls come first.  Under the
+    tracer the host's launches slow down enough that the queued kernels run
+    with idle time between them, each on its own; the tracer's timestamps
+    for graph-replayed kernels are not used, as they run the end of one
+    kernel into the start of the next."""
     import csv
     import statistics
     durs = []
@@ -235,9 +246,10 @@ def sequence_bench(args) -> int:
     timed as one HIP graph per schedule.  Every layer is its own draw (seeds
     per layer and projection, its own activations and thresholds), encoded on
     the host by a pool of worker processes and uploaded to HBM, so a step
-    streams all of its distinct weights from HBM.  When the step moves less
-    than 1 GiB the graph runs it several times over (each time the caches are
-    cleared before the timed replay)."""
+    streams all of its distinct weights from HBM.  When the step reads less
+    than the cold threshold (1 GiB) the graph runs it several times over,
+    each time on its own device copy of the layers (and the caches are
+    cleared before each timed replay)."""
     import concurrent.futures as cf
     import multiprocessing as mp
 
@@ -296,18 +308,22 @@ def sequence_bench(args) -> int:
     if fused_on:
         fys = [torch.empty(f.M, dtype=torch.int16, device=dev) for f in fused[0]]
         fws = [celty.new_workspace(f, dev) for f in fused[0]]
-    # a step smaller than the cold threshold is repeated within one graph
-    reps = max(1, -(-COLD_BYTES // max(1, stored_step)))
+    # a step that reads less than the cold threshold is repeated within one
+    # graph, each repeat on its own device copy of every layer, so that no
+    # layer is read again before COLD_BYTES of other reads
+    reps = max(1, -(-COLD_BYTES // max(1, int(alg_step))))
+    lay_r = [layers] + [[[e.clone_to() for e in L] for L in layers] for _ in range(reps - 1)]
+    fus_r = [fused] + [[[e.clone_to() for e in F_] for F_ in fused] for _ in range(reps - 1)] if fused_on else None
 
     def step_sequential(s):
         for l in range(n_layers):
-            L = layers[l]
+            L = lay_r[s % reps][l]
             for i in range(len(L)):
                 celty.celty_spmspv(L[i], xs[l][i], taus[l][i], ys[i], wss[i])
 
     def step_batched(s):
         for l in range(n_layers):
-            L = layers[l]
+            L = lay_r[s % reps][l]
             for g, w in zip(groups, bws):
                 celty.celty_spmspv_batch([L[i] for i in g], [xs[l][i] for i in g], [taus[l][i] for i in g],
                                          [ys[i] for i in g], w)
@@ -315,7 +331,7 @@ def sequence_bench(args) -> int:
     def step_fused(s):
         for l in range(n_layers):
             for j, g in enumerate(groups):
-                celty.celty_spmspv(fused[l][j], xs[l][g[0]], taus[l][g[0]], fys[j], fws[j])
+                celty.celty_spmspv(fus_r[s % reps][l][j], xs[l][g[0]], taus[l][g[0]], fys[j], fws[j])
 
     out = {"sequence": cfg, "name": c["name"], "activation_sparsity_pct": as_, "layers": n_layers,
            "distinct_layers": True, "data": "synthetic",
@@ -355,15 +371,16 @@ def sequence_bench(args) -> int:
     if fused_on and not args.no_read_floor:
         # the fused schedule's launches as plain reads of their algorithmic
         # bytes (one launch per x-group and layer, in order, distinct bytes)
-        del layers, fused
+        del layers, fused, lay_r, fus_r
         torch.cuda.empty_cache()
         sizes = [[max(16, int(sum(algs[l][i] for i in g)) // 16 * 16) for g in groups] for l in range(n_layers)]
-        buf = torch.empty(sum(sum(s) for s in sizes), dtype=torch.uint8, device=dev)
+        per_step = sum(sum(s) for s in sizes)
+        buf = torch.empty(reps * per_step, dtype=torch.uint8, device=dev)   # distinct bytes per repeat
         buf.fill_(1)
         sink = torch.empty(1024, dtype=torch.int32, device=dev)
 
         def step_read(s):
-            off = 0
+            off = (s % reps) * per_step
             for l in range(n_layers):
                 for nb in sizes[l]:
                     celty.celty_bench_stream_read(buf[off:off + nb], nb, sink, 512, 512)
@@ -558,14 +575,82 @@ def time_graph(torch, fn, steps: int, replays: int = 5, flush=None, rewarm=None)
     return float(np.median(samples)), samples
 
 
+def cold_copies(enc, p) -> int:
+    """Copies of enc to rotate so that a copy is read again only after at
+    least COLD_BYTES of other reads.  Counted in the bytes one call reads
+    (its algorithmic bytes: the active columns' entries, x and y), not in the
+    copy's stored size: a call reads the same active columns of every copy,
+    so a rotation sized by stored bytes would bring each copy's read part
+    back after far less traffic than COLD_BYTES, within reach of the
+    Infinity Cache."""
+    read = algorithmic_bytes_from_encoding(enc, p.x, p.tau)[0]
+    return max(2, -(-COLD_BYTES // max(1, int(read))))
+
+
+def time_queued(torch, fn, steps: int, replays: int = 5, flush=None, rewarm=None) -> tuple:
+    """µs per call of `steps` calls launched one after another on the launch
+    stream and all queued before the timed region starts: before each timed
+    replay (outside the events) the GPU streams reads of the cache-clearing
+    buffer for as long as the host needs to enqueue the replay (rather than
+    idling: after milliseconds of idling, the next milliseconds of this
+    kernel run measurably slower, while a plain read does not), then the
+    rewarm call and the short wait of time_graph; the GPU then runs the
+    steps back to back, with no host gap and no graph launch inside the
+    events.  (A graph replay adds a fixed cost of about 11 µs between its
+    start event and its first kernel, the same for a one-element fill as for
+    this kernel; queued launches have about 2.5 µs.)  Returns (median µs per
+    call, per-replay samples, info): info holds the host's µs per launch and
+    whether every replay's launches were all enqueued before the GPU reached
+    them (queued_ahead)."""
+    torch.cuda.synchronize()
+    n = max(1, min(steps, 50))
+    t0 = time.perf_counter()
+    for i in range(n):
+        fn(i)
+    host_us = (time.perf_counter() - t0) * 1e6 / n
+    torch.cuda.synchronize()
+    wait_us = 200.0 + 2.0 * host_us * steps
+    if flush is not None:
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        flush()
+        e.record()
+        torch.cuda.synchronize()
+        busy_us = max(1.0, s.elapsed_time(e) * 1e3)
+        reads = max(1, int(wait_us // busy_us) + 1)
+    else:   # no cache clearing (a hot run): an idle wait instead
+        busy_us, reads = wait_us, 0
+    samples, ahead = [], True
+    for _ in range(replays):
+        for _ in range(reads):
+            flush()
+        if reads == 0:
+            torch.cuda._sleep(int(wait_us * 2400))   # shader-clock cycles, at most 2.4 GHz
+        if rewarm is not None:
+            rewarm()
+        torch.cuda._sleep(200000)   # as time_graph, about 0.1 ms
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            fn(i)
+        enq = (time.perf_counter() - t0) * 1e6
+        e.record()
+        torch.cuda.synchronize()
+        ahead = ahead and enq < max(1, reads) * busy_us
+        samples.append(s.elapsed_time(e) * 1e3 / steps)
+    return float(np.median(samples)), samples, {"host_us_per_launch": round(host_us, 2), "queued_ahead": ahead,
+                                                "reads_before_each_replay": reads}
+
+
 def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool = False, flush=None) -> dict:
-    """Graph-timed µs per celty_spmspv_ex call on rotated device copies of enc
-    (at least COLD_BYTES in all, so every call streams W from HBM; with
-    flush, the caches are also cleared before every timed replay, then one
-    untimed call on a spare copy that the replay does not read re-warms the
-    code and the small buffers)."""
+    """µs per celty_spmspv_ex call (time_queued, and time_graph beside it) on
+    rotated device copies of enc (cold_copies of them, so every call streams
+    its part of W from HBM; with flush, the caches are also cleared before
+    every timed replay, then one untimed call on a spare copy that the replay
+    does not read re-warms the code and the small buffers)."""
     dev = torch.device("cuda:0")
-    ncopies = 1 if hot else max(2, -(-COLD_BYTES // stored_bytes(enc)))
+    ncopies = 1 if hot else cold_copies(enc, p)
     base = enc.to_device(dev)
     # ncopies rotated by the steps, plus one spare (the last) for the re-warm call
     copies = [base] + [base.clone_to() for _ in range(ncopies)]
@@ -586,13 +671,16 @@ def cold_spmspv(torch, celty, enc, p, launch, steps: int, warmup: int, hot: bool
     preps = [celty.PreparedSpMSpV(c, x, y, ws, launch) for c in copies]
     eager_prepared_us = time_loop(torch, lambda i: preps[i % ncopies](p.tau), steps)
     del preps
-    # the timed region: the steps captured in one HIP graph and replayed on
-    # the launch stream; one step is exactly one kernel launch
+    # the timed region: the steps launched back to back on the launch stream,
+    # all enqueued while the GPU still runs the cache-clearing reads; one step
+    # is exactly one kernel launch
     spare = copies[-1]
-    us, samples = time_graph(torch, step, steps, flush=None if hot else flush,
-                             rewarm=None if hot else (lambda: celty.celty_spmspv_ex(spare, x, p.tau, y, ws, launch)))
-    out = {"us": us, "samples": samples, "eager_us": eager_us, "eager_prepared_us": eager_prepared_us,
-           "copies": ncopies}
+    rewarm = None if hot else (lambda: celty.celty_spmspv_ex(spare, x, p.tau, y, ws, launch))
+    # first, for comparison, the same steps as one HIP graph replay
+    g_us, g_samples = time_graph(torch, step, steps, flush=None if hot else flush, rewarm=rewarm)
+    us, samples, info = time_queued(torch, step, steps, flush=None if hot else flush, rewarm=rewarm)
+    out = {"us": us, "samples": samples, "queued": info, "graph_us": g_us, "graph_samples": g_samples,
+           "eager_us": eager_us, "eager_prepared_us": eager_prepared_us, "copies": ncopies}
     del copies, base
     torch.cuda.empty_cache()
     return out
@@ -604,7 +692,7 @@ READ_SHAPES = ((256, 1024), (512, 512), (1024, 256))
 def read_floor(torch, celty, nbytes: float, steps: int, flush=None) -> dict:
     """What the memory system gives one launch that reads nbytes: the
     library's measurement reference (celty_bench_stream_read, a plain
-    streaming read) graph-timed on rotated cold buffers under the same
+    streaming read) timed on rotated cold buffers under the same
     protocol as the product, best of three launch shapes."""
     nb = max(16, int(nbytes) // 16 * 16)
     nc = max(2, -(-COLD_BYTES // nb))
@@ -614,9 +702,9 @@ def read_floor(torch, celty, nbytes: float, steps: int, flush=None) -> dict:
     sink = torch.empty(1024, dtype=torch.int32, device="cuda")
     best = None
     for blocks, threads in READ_SHAPES:
-        us, _ = time_graph(torch, lambda i: celty.celty_bench_stream_read(bufs[i % nc], nb, sink, blocks, threads),
-                           steps, replays=3, flush=flush,
-                           rewarm=lambda: celty.celty_bench_stream_read(bufs[-1], nb, sink, blocks, threads))
+        us, _, _ = time_queued(torch, lambda i: celty.celty_bench_stream_read(bufs[i % nc], nb, sink, blocks, threads),
+                               steps, replays=3, flush=flush,
+                               rewarm=lambda: celty.celty_bench_stream_read(bufs[-1], nb, sink, blocks, threads))
         if best is None or us < best[0]:
             best = (us, blocks, threads)
     del bufs
@@ -629,7 +717,7 @@ def read_floor(torch, celty, nbytes: float, steps: int, flush=None) -> dict:
 def cold_dense(torch, F, p, steps: int, hot: bool = False, flush=None) -> dict:
     """The dense reference: F.linear fp16 at batch 1 on the masked W and the
     thresholded x, same cold rotation, cache clearing, re-warm call on a spare
-    copy and graph timing."""
+    copy and queued-launch timing."""
     dev = torch.device("cuda:0")
     M, K = p.W.shape
     Wf = torch.from_numpy(np.where(p.mask != 0, p.W, np.float16(0))).to(dev)
@@ -638,18 +726,14 @@ def cold_dense(torch, F, p, steps: int, hot: bool = False, flush=None) -> dict:
     xd = torch.from_numpy(np.where(np.abs(p.x.astype(np.float32)) > p.tau, p.x, np.float16(0))).to(dev)[None]
     for i in range(20):
         F.linear(xd, dcopies[i % nd])
-    try:
-        dense_us, _ = time_graph(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps,
+    dense_us, _, _ = time_queued(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps,
                                  flush=None if hot else flush,
                                  rewarm=None if hot else (lambda: F.linear(xd, dcopies[-1])))
-        dense_mode = "graph"
-    except Exception:
-        dense_us, dense_mode = time_loop(torch, lambda i: F.linear(xd, dcopies[i % nd]), steps), "eager"
     del dcopies, Wf
     torch.cuda.empty_cache()
     return {"us": round(dense_us, 3), "GBps": round((2 * M * K + 2 * K + 2 * M) / dense_us / 1e3, 1),
             "op": "torch.nn.functional.linear fp16, batch 1 (hipBLASLt/rocBLAS)", "copies": nd,
-            "timing": dense_mode}
+            "timing": "queued launches, as the SpMSpV"}
 
 
 VARIANT_SHAPES = ((4096, 4096, 70, 70), (4096, 4096, 30, 30), (5120, 5120, 60, 60), (13824, 5120, 60, 60),
@@ -662,8 +746,8 @@ def variant_study(args) -> int:
     XOR-swizzled tile, 16-bit row offsets (no reconstruction) and the runs in
     lane-interleaved order.  Per shape: the three encodings on rotated cold
     copies, the four y checked bit-equal, then three rounds (alternating
-    order) of graph timing with the caches cleared before every replay; one
-    JSON line per shape with the median µs of each variant."""
+    order) of queued-launch timing with the caches cleared before every
+    replay; one JSON line per shape with the median µs of each variant."""
     import torch
 
     import paper_2608_01536_amd as celty
@@ -682,7 +766,7 @@ def variant_study(args) -> int:
         for k, e in encs.items():
             base = e.to_device(dev)
             # rotated copies, plus a spare (the last) for the re-warm call
-            copies[k] = [base] + [base.clone_to() for _ in range(max(2, -(-COLD_BYTES // stored_bytes(e))))]
+            copies[k] = [base] + [base.clone_to() for _ in range(cold_copies(e, p))]
         copies["swizzle"] = copies["rlc"]
         launch = {v: (0, 0, 0, 1 if v == "swizzle" else 0) for v in names}
         x = torch.from_numpy(p.x.view(np.int16)).to(dev)
@@ -699,10 +783,11 @@ def variant_study(args) -> int:
             for v in (names if rnd % 2 == 0 else names[::-1]):
                 cs = copies[v]
                 n_rot = len(cs) - 1
-                us, _ = time_graph(torch, lambda i, cs=cs, v=v: celty.celty_spmspv_ex(cs[i % n_rot], x, p.tau, y, wsb,
-                                                                                     launch[v]),
-                                   args.steps, replays=3, flush=flush,
-                                   rewarm=lambda cs=cs, v=v: celty.celty_spmspv_ex(cs[-1], x, p.tau, y, wsb, launch[v]))
+                us, _, _ = time_queued(torch, lambda i, cs=cs, v=v: celty.celty_spmspv_ex(cs[i % n_rot], x, p.tau, y,
+                                                                                         wsb, launch[v]),
+                                       args.steps, replays=3, flush=flush,
+                                       rewarm=lambda cs=cs, v=v: celty.celty_spmspv_ex(cs[-1], x, p.tau, y, wsb,
+                                                                                       launch[v]))
                 res[v].append(us)
         b_alg = algorithmic_bytes_from_encoding(encs["rlc"], p.x, p.tau)[0]
         med = {v: round(float(np.median(res[v])), 3) for v in names}
@@ -797,6 +882,7 @@ def cpu_baseline(p, budget_s: float) -> dict:
 
 
 def main() -> int:
+    global COLD_BYTES
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
@@ -817,6 +903,9 @@ def main() -> int:
                     help="outlier input features: per-feature scales exp(sigma*N(0,1)) on W's columns and x, "
                          "per-row magnitude pruning (0 = the uniform-mask workload)")
     ap.add_argument("--hot", action="store_true", help="reuse one copy (cache-resident; diagnostic)")
+    ap.add_argument("--cold-bytes", type=int, default=COLD_BYTES,
+                    help="reads between two reads of the same data in the timed loops, and the size of the "
+                         "cache-clearing read before each timed replay (default 1 GiB)")
     ap.add_argument("--layout", choices=("rlc", "rows16", "interleaved"), default="rlc",
                     help="row encoding of the matrix: the paper's 4-bit runs (default), 16-bit row offsets "
                          "(decode-free), or the runs in lane-interleaved order")
@@ -844,6 +933,7 @@ def main() -> int:
     ap.add_argument("--encode-throughput", action="store_true",
                     help="host only: encoder throughput on the benchmark matrices")
     args = ap.parse_args()
+    COLD_BYTES = max(256 << 20, args.cold_bytes // 4096 * 4096)
     if args.copy_calibration:
         return copy_calibration()
     if args.format_study:
@@ -920,12 +1010,13 @@ def main() -> int:
     run = cold_spmspv(torch, celty, enc, p, launch, args.steps, args.warmup, args.hot, flush=flush)
     us_step, samples, eager_us, ncopies = run["us"], run["samples"], run["eager_us"], run["copies"]
     us_kernel = us_step
-    print(f"[bench] timed: {us_step:.3f} us/step (graph), eager {eager_us:.2f} us/call", file=sys.stderr, flush=True)
+    print(f"[bench] timed: {us_step:.3f} us/step (queued launches), {run['graph_us']:.3f} (graph replay), "
+          f"eager {eager_us:.2f} us/call", file=sys.stderr, flush=True)
 
     # floor: a near-empty kernel (one-element fill) under the same timing
     tiny = torch.zeros(1, device=dev)
     floor_wall = time_loop(torch, lambda i: tiny.fill_(1.0), args.steps)
-    floor_kernel, _ = time_graph(torch, lambda i: tiny.fill_(1.0), args.steps)
+    floor_kernel, _, _ = time_queued(torch, lambda i: tiny.fill_(1.0), args.steps, flush=flush)
 
     dense = None if args.no_dense else cold_dense(torch, F, p, args.steps, args.hot, flush=flush)
     floor_read = None if (args.hot or args.no_read_floor) else read_floor(torch, celty, b_alg, args.steps, flush)
@@ -978,7 +1069,11 @@ def main() -> int:
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
                      "kernel_us": round(us_kernel, 3), "kernel_us_replays": [round(v, 3) for v in samples],
                      "bytes_per_launch": b_alg,
-                     "timing": "HIP events around a graph replay of the K steps on the launch stream",
+                     "timing": "HIP events on the launch stream around the K steps, launched back to back, "
+                               "all enqueued before the GPU reaches the start event",
+                     "queued": run["queued"],
+                     "graph_replay_us": round(run["graph_us"], 3),
+                     "graph_replay_us_replays": [round(v, 3) for v in run["graph_samples"]],
                      "kernel_trace": None if ktrace is None else {
                          "mean_us": round(ktrace["mean_ns"] / 1e3, 3), "median_us": round(ktrace["median_ns"] / 1e3, 3),
                          "frac_mean": round(b_alg / ktrace["mean_ns"] / PEAK_HBM_GBPS, 4),
@@ -987,7 +1082,7 @@ def main() -> int:
                          "source": os.path.relpath(kernel_trace_file(workload_key), ROOT)}},
         "eager_us_per_call": round(eager_us, 3),
         "eager_us_per_call_prepared": round(run["eager_prepared_us"], 3),
-        "launch_floor": {"graph_us": round(floor_kernel, 3), "eager_us": round(floor_wall, 3),
+        "launch_floor": {"queued_us": round(floor_kernel, 3), "eager_us": round(floor_wall, 3),
                          "op": "one-element torch fill kernel"},
         "read_floor": None if floor_read is None else dict(
             floor_read, kernel_vs_floor=round(floor_read["us"] / us_step, 3),

@@ -31,3 +31,20 @@ def test_kernel_code_hash_ignores_comments_only():
     assert bench.kernel_source_code(src.replace("// note", "// other note\n\n")) == code
     assert bench.kernel_source_code(src.replace("a = 1", "a = 2")) != code
     assert bench.kernel_source_code('s = "a\\"b // c";') == 's = "a\\"b // c";'
+
+
+@pytest.mark.parametrize("ws,as_", [(70, 70), (50, 0), (30, 90)])
+def test_cold_rotation_counts_the_bytes_a_call_reads(ws, as_):
+    # a copy is read again only after COLD_BYTES of reads of the other
+    # copies: the rotation is sized by the bytes one call reads (its active
+    # columns), which at high activation sparsity is far below the copy's
+    # stored size
+    p = workloads.random_small(ws + as_, 600, 500, ws=ws, as_=as_)
+    enc = celty.celty_encode(p.W, p.mask, 128)
+    read = bench.algorithmic_bytes_from_encoding(enc, p.x, p.tau)[0]
+    n = bench.cold_copies(enc, p)
+    assert n * read >= bench.COLD_BYTES
+    assert (n - 1) * read < bench.COLD_BYTES
+    if as_ > 0:
+        assert read < bench.stored_bytes(enc)
+        assert n > -(-bench.COLD_BYTES // bench.stored_bytes(enc))
