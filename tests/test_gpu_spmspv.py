@@ -6,7 +6,8 @@
   all-inactive x (every row +0), empty matrix;
 * edge shapes: M < R, M % R != 0, K = 1, K not a multiple of 64, R = 1;
 * every launch shape gives the same answer within tolerance;
-* the workspace is left zero-filled by every call; y is fully overwritten;
+* the workspace is left zero-filled by every call, also by calls queued
+  back to back with no host synchronisation; y is fully overwritten;
 * full-size runs of all five benchmark configurations, and of the paper's
   kernel shapes at 30/50/70 % dual sparsity, in the launch shape the
   benchmark uses.
@@ -272,6 +273,33 @@ def test_repeated_calls_share_a_workspace(celty, torch_dev):
     assert int(ws.count_nonzero()) == 0
     for y in outs:
         assert ref.rel_error(y.cpu().numpy().view(np.float16).astype(np.float64), want) <= TOL
+
+
+@pytest.mark.parametrize("M,K,ws,as_", [(4096, 4096, 70, 70), (8192, 8192, 50, 60)])
+def test_queued_calls_share_a_workspace(celty, torch_dev, M, K, ws, as_):
+    # calls enqueued while the GPU is still busy, so they run back to back
+    # with no host synchronisation between them: each must find the merge
+    # words the previous one left zero, and its y must equal a lone call's
+    # bit for bit (the sums are exact integers, whatever the slices' order)
+    torch, dev = torch_dev
+    p = workloads.make_problem(2, M, K, ws, as_, "laplace", seed=3, proj=workloads.PROJ_IDS["w"])
+    enc = celty.celty_encode(p.W, p.mask, celty.default_tile_rows(M, K))
+    Wd = enc.to_device(dev)
+    copies = [Wd, Wd.clone_to()]
+    xt = torch.from_numpy(p.x.view(np.int16)).to(dev)
+    ws_ = celty.new_workspace(Wd, dev)
+    y0 = torch.empty(M, dtype=torch.int16, device=dev)
+    celty.celty_spmspv(Wd, xt, p.tau, y0, ws_)
+    torch.cuda.synchronize()
+    ys = [torch.full((M,), 0x7C01, dtype=torch.int16, device=dev) for _ in range(32)]
+    _note(f"queued calls {M}x{K} ws{ws} as{as_}")
+    torch.cuda._sleep(2000000)   # about 1 ms of device time: the host enqueues every call meanwhile
+    for i, y in enumerate(ys):
+        celty.celty_spmspv(copies[i % 2], xt, p.tau, y, ws_)
+    torch.cuda.synchronize()
+    assert int(ws_.count_nonzero()) == 0
+    assert all(torch.equal(y, y0) for y in ys)
+    _check(y0.cpu().numpy().view(np.float16), p.W, p.mask, p.x, p.tau)
 
 
 # --------------------------------------------------------------------------
