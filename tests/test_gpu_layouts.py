@@ -11,8 +11,9 @@ is also checked against the fp64 definition (the oracle) within 2e-3.  Shapes
 cover several tiles and a ragged last tile, one and several column slices,
 segments of more than 64 groups (several interleave chunks, wavefront ranges
 that start inside a segment), 2 to 16 wavefronts, tau < 0, NaN activations,
-an all-inactive x, and the identity pattern (single-term rows, bit-exact
-against x itself).
+an all-inactive x, the identity pattern (single-term rows, bit-exact
+against x itself), and the full-size 28672 x 8192 and 13824 x 5120 problems
+in the automatic launch shape.
 """
 import numpy as np
 import pytest
@@ -93,6 +94,21 @@ def test_variant_matches_rlc_kernel_and_oracle(celty, torch_dev, variant, label,
     _note(f"{variant} {label}: {M}x{K} ws{ws} as{as_} R={R} launch=({cols},{waves})")
     p = workloads.make_problem(2, M, K, ws, as_, "laplace", seed=M + K + ws, proj=workloads.PROJ_IDS["w"])
     y, y0 = _both(celty, torch_dev, variant, p.W, p.mask, p.x, p.tau, R, cols, waves)
+    assert np.array_equal(y, y0), f"{int(np.count_nonzero(y != y0))} rows differ from the RLC kernel"
+    want = ref.spmspv_dense_fp64(p.W, p.mask, p.x, p.tau)
+    err = ref.rel_error(y.view(np.float16).astype(np.float64), want)
+    _note(f"  rel_err={err:.3e}")
+    assert err <= TOL, err
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("M,K,ws,as_", [(28672, 8192, 50, 40), (13824, 5120, 60, 60)])
+def test_variant_full_size_in_the_automatic_shape(celty, torch_dev, variant, M, K, ws, as_):
+    # the variant study's largest problems, in the launch shape bench.py uses
+    _note(f"{variant} full size {M}x{K} ws{ws} as{as_}")
+    p = workloads.make_problem(2, M, K, ws, as_, "laplace", seed=0, proj=workloads.PROJ_IDS["w"])
+    R = celty.default_tile_rows(M, K)
+    y, y0 = _both(celty, torch_dev, variant, p.W, p.mask, p.x, p.tau, R)
     assert np.array_equal(y, y0), f"{int(np.count_nonzero(y != y0))} rows differ from the RLC kernel"
     want = ref.spmspv_dense_fp64(p.W, p.mask, p.x, p.tau)
     err = ref.rel_error(y.view(np.float16).astype(np.float64), want)
